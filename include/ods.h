@@ -1,0 +1,208 @@
+/*
+ * ods.h -- C ABI of the operator-level-disaggregated (ODS) decode hot path on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The paper models one decode step as a fixed, ordered sequence of kernels
+ * o_1..o_N (Appendix A.1) and a serving stage as a contiguous slice of the
+ * operator sequence of a repeating partition block: stage j holds operators
+ * q_{j-1}+1 .. q_j (Section 4, "Partition-block abstraction"; Appendix B.1).
+ * Stages exchange an activation interface A_j at each boundary (Appendix B.3,
+ * the stage-latency and transfer-latency equations), a worker loads only its
+ * assigned components and state, buffers are bound once with only token,
+ * position and KV metadata changing between steps, and one native call
+ * enqueues a whole per-step action sequence (Section 6 and its "Single native
+ * submission" optimisation). This library is that native call for one GPU.
+ *
+ * Operator index space. A block of layers is numbered globally, layer after
+ * layer; indices are 0-based and ranges half-open, so the paper's stage j is
+ * [q_{j-1}, q_j). Per layer (local index):
+ *
+ *   dense layer (10 ops)                  MoE layer (14 ops)
+ *   0 attn_norm        resid -> xn        0..6 as in the dense layer
+ *   1 qkv_proj         xn -> qkv          7  router          hn -> logits
+ *   2 rope             qkv -> qkv         8  topk_softmax    logits -> topk_ids, topk_w
+ *   3 kv_append        qkv -> KV pool     9  moe_permute     hn, topk_ids -> xp, perm,
+ *   4 attn_core        qkv, pool -> o                            slot_pos, expert_off
+ *   5 o_proj_residual  o, resid -> resid  10 expert_gate_up  xp -> gu_p
+ *   6 ffn_norm         resid -> hn        11 silu_mul        gu_p -> act_p
+ *   7 gate_up          hn -> gu           12 expert_down     act_p -> yp
+ *   8 silu_mul         gu -> act          13 moe_combine_residual
+ *   9 down_residual    act, resid -> resid                   yp, topk_w, slot_pos, resid -> resid
+ *
+ * Attention-FFN disaggregation cuts every layer at local 6; core-attention
+ * disaggregation isolates [3, 5); the colocated template is [0, N_block)
+ * (Section 4, "Design-space expressiveness").
+ *
+ * Numerics (the paper leaves the layer's arithmetic unspecified; these are the
+ * library's conventions): bf16 storage, fp32 accumulation. RMSNorm
+ * x * (mean(x^2) + eps)^-1/2 * gain. RoPE rotate-half pairs (i, i + d/2) at
+ * position ctx - 1, angle (ctx - 1) * theta^(-2i/d) evaluated in double.
+ * Attention softmax(q K^T / sqrt(d)) V over keys [ctx - window, ctx - 1]
+ * (window 0: all keys); query head h reads KV head h / (n_q / n_kv).
+ * SwiGLU silu(gate) * up. Routing: top-k of the fp32 router logits (ties go to
+ * the lower expert index), weights = softmax over the chosen k. Every live
+ * buffer is rounded to bf16 (round-to-nearest-even) except logits and routing
+ * weights (fp32) and indices (int32).
+ *
+ * Ownership and errors. The caller owns all memory and the stream. The library
+ * never allocates, frees, synchronises, or changes the current device, and
+ * keeps no state between calls. Every argument is checked on the host before
+ * anything is enqueued: a non-OK status means nothing was enqueued, except
+ * ODS_EHIP, which reports a launch failure after earlier kernels of the same
+ * call were enqueued. Device faults surface at the caller's synchronisation.
+ * All device pointers must be 16-byte aligned. Calls are thread-safe;
+ * ods_last_error() is per thread.
+ */
+#ifndef ODS_H
+#define ODS_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ODS_OK = 0,
+  ODS_EINVAL = -1,        /* null / misaligned pointer, negative size, bad enum */
+  ODS_ERANGE = -2,        /* operator range or context outside its bounds */
+  ODS_ENOMEM = -3,        /* KV pool or workspace too small */
+  ODS_EUNSUPPORTED = -4,  /* shape the kernels do not implement */
+  ODS_EHIP = -5           /* HIP runtime reported an error while enqueuing */
+} ods_status;
+
+#define ODS_PAGE_TOKENS 16
+
+/* Shape of one decoder layer. n_experts == 0 selects a dense SwiGLU FFN of
+ * width ffn; otherwise a top_k-of-n_experts MoE with per-expert width moe_ffn.
+ * window == 0 selects full attention, window > 0 a sliding window of that many
+ * most recent tokens (the decoded token included).
+ * Supported: head_dim in {64, 128}; n_q a multiple of n_kv with n_q / n_kv <= 16;
+ * hidden, ffn, moe_ffn multiples of 8; n_experts <= 256; 1 <= top_k <= n_experts. */
+typedef struct {
+  int32_t hidden, n_q, n_kv, head_dim;
+  int32_t ffn;
+  int32_t n_experts, top_k, moe_ffn;
+  int32_t window;
+  float rope_theta, rms_eps;
+} ods_layer_cfg;
+
+/* One layer's device-resident weights (bf16, row-major "out x in") and KV pool.
+ *   g_attn, g_ffn  [hidden]
+ *   w_qkv          [(n_q + 2 n_kv) head_dim, hidden]   q heads, then k heads, then v heads
+ *   w_o            [hidden, n_q head_dim]
+ *   dense: w_gate_up [2 ffn, hidden] (gate rows, then up rows); w_down [hidden, ffn]
+ *   MoE:   w_router [n_experts, hidden]; w_gate_up [n_experts, 2 moe_ffn, hidden];
+ *          w_down [n_experts, hidden, moe_ffn]
+ *   kv_pool  [pool_pages][2][n_kv][16 * head_dim] bf16. Block (page, 0, g) holds the
+ *            keys of 16 token slots row-major (slot t, dim i at t * head_dim + i);
+ *            block (page, 1, g) holds the values dim-major (dim i, slot t at i * 16 + t).
+ *            Token position t of a sequence lives in page page_table[b][t / 16],
+ *            slot t % 16. Every block is 16 * head_dim * 2 bytes, contiguous. */
+typedef struct {
+  ods_layer_cfg cfg;
+  const void *g_attn, *w_qkv, *w_o, *g_ffn, *w_gate_up, *w_down, *w_router;
+  void *kv_pool;
+  int64_t pool_pages;
+} ods_layer;
+
+/* A partition block: n_layers layers whose operators are numbered consecutively.
+ * All layers share one batch, page table and live set. */
+typedef struct {
+  int32_t n_layers;
+  const ods_layer *layers;
+} ods_block;
+
+/* Per-step metadata (device pointers). ctx_lens[b] counts the keys sequence b
+ * attends to, the token being decoded included, so that token's position is
+ * ctx_lens[b] - 1; valid values are 1 .. max_pages * 16 (larger values are
+ * clamped, values < 1 make the row a no-op for attention and KV append).
+ * page_table [batch][max_pages] int32, -1 for unused entries; page ids outside
+ * [0, pool_pages) are skipped by the kernels. split_pages chooses the pages
+ * per split-K work item of attn_core (0: library choice). */
+typedef struct {
+  int32_t batch, max_pages;
+  const int32_t *ctx_lens;
+  const int32_t *page_table;
+  int32_t split_pages;
+} ods_batch;
+
+/* Live buffers (the activation interface at any cut), device, caller-allocated.
+ * Sizes per ods_live_bytes(). Only buffers read or written by the operators of
+ * a call's range need to be non-null.
+ *   resid [B, H] bf16 (updated in place by o_proj_residual, down_residual,
+ *   moe_combine_residual); xn, hn [B, H]; qkv [B, (n_q + 2 n_kv) d]; o [B, n_q d];
+ *   gu [B, 2F]; act [B, F]; logits [B, E] fp32; topk_ids [B, k] int32;
+ *   topk_w [B, k] fp32; perm [B k] (sorted position -> token * k + slot);
+ *   slot_pos [B k] (token * k + slot -> sorted position); expert_off [E + 1];
+ *   xp [B k, H]; gu_p [B k, 2 I]; act_p [B k, I]; yp [B k, H] (all bf16);
+ *   ws: scratch of at least ods_workspace_bytes() bytes. */
+typedef struct {
+  void *resid, *xn, *qkv, *o, *hn, *gu, *act;
+  float *logits, *topk_w;
+  int32_t *topk_ids, *perm, *slot_pos, *expert_off;
+  void *xp, *gu_p, *act_p, *yp;
+  void *ws;
+  size_t ws_bytes;
+} ods_state;
+
+typedef enum {
+  ODS_BUF_RESID = 0, ODS_BUF_XN, ODS_BUF_QKV, ODS_BUF_O, ODS_BUF_HN, ODS_BUF_GU, ODS_BUF_ACT,
+  ODS_BUF_LOGITS, ODS_BUF_TOPK_W, ODS_BUF_TOPK_IDS, ODS_BUF_PERM, ODS_BUF_SLOT_POS,
+  ODS_BUF_EXPERT_OFF, ODS_BUF_XP, ODS_BUF_GU_P, ODS_BUF_ACT_P, ODS_BUF_YP, ODS_BUF_COUNT
+} ods_buffer;
+
+/* Host-only page allocation for one step's batch (no device work). The pool's
+ * page ids [0, pool_pages) are shuffled by a Fisher-Yates pass driven by
+ * splitmix64(seed) (for i = P-1 down to 1, swap entries i and next() mod (i+1));
+ * sequence b then takes the next ceil(ctx_lens_host[b] / 16) shuffled ids, in
+ * batch order. Writes page_table_host [batch][max_pages] (caller memory), -1 in
+ * unused entries. ODS_ENOMEM if the batch needs more than pool_pages pages,
+ * ODS_ERANGE if a sequence needs more than max_pages, ODS_EINVAL for null
+ * pointers or non-positive ctx. The paged cache itself follows the paper's use
+ * of paged KV memory in its serving engine (Section 6). */
+ods_status ods_kv_alloc(int64_t pool_pages, const int32_t *ctx_lens_host, int32_t batch,
+                        uint64_t seed, int32_t max_pages, int32_t *page_table_host);
+
+/* Bytes of one layer's KV pool of pool_pages pages (0 for an invalid cfg). */
+size_t ods_kv_pool_bytes(const ods_layer_cfg *cfg, int64_t pool_pages);
+
+/* Bytes of live buffer `which` for this block at this batch size (the maximum
+ * over the block's layers; 0 when no layer uses the buffer). */
+size_t ods_live_bytes(const ods_block *blk, int32_t batch, ods_buffer which);
+
+/* Minimum ods_state.ws_bytes for any operator range of this block and batch. */
+size_t ods_workspace_bytes(const ods_block *blk, const ods_batch *batch);
+
+/* Number of operators of the block (sum over layers of 10 or 14); < 0 on error. */
+int32_t ods_block_num_ops(const ods_block *blk);
+
+/* Static name of global operator `op` ("attn_core", ...), NULL if out of range. */
+const char *ods_op_name(const ods_block *blk, int32_t op);
+
+/* Enqueue operators [op_begin, op_end) of the block on `stream` (one native
+ * submission for one stage; Section 6). Adjacent operators inside the range
+ * may be fused; every buffer of the live set at op_end is materialised, so a
+ * block run as any sequence of contiguous ranges computes the same step.
+ * ODS_ERANGE unless 0 <= op_begin < op_end <= ods_block_num_ops(). */
+ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_end,
+                             const ods_batch *batch, ods_state *state, hipStream_t stream);
+
+/* The attention stage of layer `layer`: its operators 0..5 (attention-FFN
+ * disaggregation's attention side; Section 2, "Attention-FFN Disaggregation"). */
+ods_status ods_attn_stage(const ods_block *blk, int32_t layer, const ods_batch *batch,
+                          ods_state *state, hipStream_t stream);
+
+/* The FFN / MoE stage of layer `layer`: its operators 6 .. end of layer. */
+ods_status ods_ffn_stage(const ods_block *blk, int32_t layer, const ods_batch *batch,
+                         ods_state *state, hipStream_t stream);
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char *ods_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ODS_H */

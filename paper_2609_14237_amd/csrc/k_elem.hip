@@ -1,0 +1,130 @@
+// Row-wise and elementwise operators of the decode layer: RMSNorm, RoPE with
+// KV-cache append, SiLU(gate) * up. All are a few MB per step at the largest
+// batch; they stream rows with 16-byte vector accesses, one block per row.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace ods {
+
+namespace {
+
+// out[r] = x[r] * (mean(x[r]^2) + eps)^(-1/2) * gain, fp32 math, bf16 out.
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t *x, const uint16_t *gain,
+                                                      uint16_t *out, int H, float eps) {
+  __shared__ float red[4];
+  const int64_t row = blockIdx.x;
+  const u32x4 *xr = (const u32x4 *)(x + row * H);
+  const int nvec = H / 8;
+  float ss = 0.f;
+  for (int v = threadIdx.x; v < nvec; v += 256) {
+    const u32x4 w = xr[v];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float a = bf_lo(w[j]), b = bf_hi(w[j]);
+      ss += a * a + b * b;
+    }
+  }
+  ss = block_sum_256(ss, red);
+  const float inv = rsqrtf(ss / (float)H + eps);
+  u32x4 *orow = (u32x4 *)(out + row * H);
+  const u32x4 *g = (const u32x4 *)gain;
+  for (int v = threadIdx.x; v < nvec; v += 256) {
+    const u32x4 w = xr[v], gw = g[v];
+    u32x4 o;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      o[j] = pack2(bf_lo(w[j]) * inv * bf_lo(gw[j]), bf_hi(w[j]) * inv * bf_hi(gw[j]));
+    orow[v] = o;
+  }
+}
+
+// One block per sequence. RoPE (rotate-half) of the n_q + n_kv heads of
+// qkv[b] at position ctx[b] - 1, in place, and/or store of k, v into the page
+// slot of that position. cos/sin are computed once per pair index in double.
+__global__ __launch_bounds__(256) void rope_append_kernel(uint16_t *qkv, int n_q, int n_kv, int D,
+                                                          float theta, const int32_t *ctx_lens,
+                                                          const int32_t *page_table, int max_pages,
+                                                          uint16_t *pool, int64_t pool_pages,
+                                                          int do_rope, int do_append) {
+  __shared__ float cs[64], sn[64];
+  const int b = blockIdx.x;
+  const int ctx = ctx_lens[b];
+  if (ctx < 1) return;
+  const int p = min(ctx, max_pages * kPage) - 1;
+  const int half = D / 2;
+  uint16_t *row = qkv + (int64_t)b * (n_q + 2 * n_kv) * D;
+  if (do_rope) {
+    if (threadIdx.x < half) {
+      const double inv = pow((double)theta, -2.0 * (double)threadIdx.x / (double)D);
+      const double a = (double)p * inv;
+      cs[threadIdx.x] = (float)cos(a);
+      sn[threadIdx.x] = (float)sin(a);
+    }
+    __syncthreads();
+    const int pairs = (n_q + n_kv) * half;
+    for (int t = threadIdx.x; t < pairs; t += 256) {
+      const int h = t / half, i = t % half;
+      uint16_t *u = row + h * D;
+      const float x0 = bf2f(u[i]), x1 = bf2f(u[i + half]);
+      u[i] = f2bf(x0 * cs[i] - x1 * sn[i]);
+      u[i + half] = f2bf(x1 * cs[i] + x0 * sn[i]);
+    }
+    __syncthreads();
+  }
+  if (do_append) {
+    const int page = page_table[(int64_t)b * max_pages + p / kPage];
+    if (page < 0 || page >= pool_pages) return;
+    const int slot = p % kPage;
+    const int64_t blk = (int64_t)kPage * D;
+    uint16_t *kbase = pool + (int64_t)page * 2 * n_kv * blk;
+    uint16_t *vbase = kbase + n_kv * blk;
+    const uint16_t *k = row + n_q * D, *v = row + (n_q + n_kv) * D;
+    for (int t = threadIdx.x; t < n_kv * D; t += 256) {
+      const int g = t / D, i = t % D;
+      kbase[g * blk + slot * D + i] = k[t];
+      vbase[g * blk + i * kPage + slot] = v[t];
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void silu_mul_kernel(const uint16_t *gu, uint16_t *act, int F, int vblocks) {
+  const int64_t row = blockIdx.x / vblocks;
+  const int v = (blockIdx.x % vblocks) * 256 + threadIdx.x;  // 8-element vector index
+  if (v * 8 >= F) return;
+  const u32x4 g = *(const u32x4 *)(gu + row * 2 * F + v * 8);
+  const u32x4 u = *(const u32x4 *)(gu + row * 2 * F + F + v * 8);
+  u32x4 o;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    o[j] = pack2(silu(bf_lo(g[j])) * bf_lo(u[j]), silu(bf_hi(g[j])) * bf_hi(u[j]));
+  *(u32x4 *)(act + row * F + v * 8) = o;
+}
+
+}  // namespace
+
+hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gain, uint16_t *out, int rows, int H,
+                          float eps, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(rows), dim3(256), 0, s, x, gain, out, H, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_append(uint16_t *qkv, int B, int n_q, int n_kv, int D, float theta,
+                              const int32_t *ctx_lens, const int32_t *page_table, int max_pages,
+                              uint16_t *pool, int64_t pool_pages, bool do_rope, bool do_append,
+                              hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_append_kernel, dim3(B), dim3(256), 0, s, qkv, n_q, n_kv, D, theta, ctx_lens,
+                     page_table, max_pages, pool, pool_pages, (int)do_rope, (int)do_append);
+  return hipGetLastError();
+}
+
+hipError_t launch_silu_mul(const uint16_t *gu, uint16_t *act, int rows, int F, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  const int vblocks = (F / 8 + 255) / 256;
+  hipLaunchKernelGGL(silu_mul_kernel, dim3((unsigned)((int64_t)rows * vblocks)), dim3(256), 0, s, gu, act, F,
+                     vblocks);
+  return hipGetLastError();
+}
+
+}  // namespace ods

@@ -1,0 +1,258 @@
+// bf16 MFMA GEMM for the decode projections, the SwiGLU FFN and the grouped
+// expert GEMMs: C[m, n] = sum_k A[m, k] * B[n, k] (both operands K-contiguous,
+// "out x in" weights), fp32 accumulation, fused epilogues.
+//
+// Tiling: 256 threads = 4 waves; block tile BM x BN outputs, K step 64; LDS
+// double buffering (global loads of step k+1 are in flight while step k runs
+// on the matrix cores). MFMA 16x16x32 bf16: lane l holds A[m = l%16][8 k's
+// starting at (l/16)*8] and B[same k's][n = l%16]; the 16x16 fp32 result puts
+// rows (l/16)*4 .. +3 of column l%16 in lane l.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace ods {
+
+namespace {
+
+constexpr int BK = 64;
+constexpr int LDS_STRIDE = BK + 8;  // elements; 16-byte row pad against bank conflicts
+
+template <int BM, int BN, int WM, int WN, int EPI, bool PARTIAL>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs p) {
+  constexpr bool SILU = EPI == EPI_SILU;
+  constexpr int BNL = SILU ? 2 * BN : BN;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int TM = WTM / 16, TN = WTN / 16;
+  constexpr int NB = SILU ? 2 * TN : TN;  // B fragments (gate then up) per wave
+  constexpr int A_CHUNKS = BM * (BK / 8) / 256;
+  constexpr int B_CHUNKS = BNL * (BK / 8) / 256;
+  static_assert(WM * WN == 4, "4 waves");
+  static_assert(A_CHUNKS * 256 == BM * (BK / 8) && B_CHUNKS * 256 == BNL * (BK / 8), "tile");
+
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDS_STRIDE];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BNL * LDS_STRIDE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int n0 = blockIdx.x * BN;
+
+  int m_begin = 0, m_end = p.M;
+  const uint16_t *Bg = p.B;
+  int k_begin = 0, k_end = p.K;
+  int split = 0;
+  if (p.group_off) {
+    const int g = blockIdx.z;
+    m_begin = max(0, p.group_off[g]);        // offsets come from device memory:
+    m_end = min(p.M, p.group_off[g + 1]);    // never step outside the M rows
+    Bg += (int64_t)g * p.b_group_stride;
+  } else if (PARTIAL) {
+    split = blockIdx.z;
+    const int steps = (p.K + BK - 1) / BK;
+    const int per = (steps + p.splits - 1) / p.splits;
+    k_begin = split * per * BK;
+    k_end = min(p.K, k_begin + per * BK);
+  }
+  if (k_begin >= k_end && !PARTIAL) return;
+
+  // Global row of each B-tile row this thread loads (-1: outside N).
+  int64_t b_row_off[B_CHUNKS];
+#pragma unroll
+  for (int i = 0; i < B_CHUNKS; ++i) {
+    const int r = (tid + i * 256) >> 3;
+    int n, row;
+    if (SILU) {
+      n = n0 + (r % BN);
+      row = (r < BN) ? n : p.n_up + n;
+    } else {
+      n = n0 + r;
+      row = n;
+    }
+    b_row_off[i] = (n < p.N) ? (int64_t)row * p.ldb : -1;
+  }
+
+  for (int m0 = m_begin + blockIdx.y * BM; m0 < m_end; m0 += gridDim.y * BM) {
+    f32x4 acc[TM][NB];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    u32x4 ra[A_CHUNKS], rb[B_CHUNKS];
+    auto load = [&](int k0) {
+#pragma unroll
+      for (int i = 0; i < A_CHUNKS; ++i) {
+        const int c = tid + i * 256, r = c >> 3, kc = (c & 7) * 8;
+        const int m = m0 + r, k = k0 + kc;
+        ra[i] = (m < m_end && k < k_end) ? *(const u32x4 *)(p.A + (int64_t)m * p.lda + k)
+                                         : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int i = 0; i < B_CHUNKS; ++i) {
+        const int c = tid + i * 256, kc = (c & 7) * 8;
+        const int k = k0 + kc;
+        rb[i] = (b_row_off[i] >= 0 && k < k_end) ? *(const u32x4 *)(Bg + b_row_off[i] + k)
+                                                 : u32x4{0u, 0u, 0u, 0u};
+      }
+    };
+    auto store = [&](int buf) {
+#pragma unroll
+      for (int i = 0; i < A_CHUNKS; ++i) {
+        const int c = tid + i * 256, r = c >> 3, kc = (c & 7) * 8;
+        *(u32x4 *)&As[buf][r * LDS_STRIDE + kc] = ra[i];
+      }
+#pragma unroll
+      for (int i = 0; i < B_CHUNKS; ++i) {
+        const int c = tid + i * 256, r = c >> 3, kc = (c & 7) * 8;
+        *(u32x4 *)&Bs[buf][r * LDS_STRIDE + kc] = rb[i];
+      }
+    };
+
+    const int nk = (k_end - k_begin + BK - 1) / BK;
+    if (nk > 0) {
+      load(k_begin);
+      store(0);
+    }
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const int cur = kt & 1;
+      if (kt + 1 < nk) load(k_begin + (kt + 1) * BK);
+#pragma unroll
+      for (int ks = 0; ks < BK / 32; ++ks) {
+        bf16x8 af[TM], bfr[NB];
+        const int col = ks * 32 + (lane >> 4) * 8;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int r = wm * WTM + i * 16 + (lane & 15);
+          af[i] = __builtin_bit_cast(bf16x8, *(const u32x4 *)&As[cur][r * LDS_STRIDE + col]);
+        }
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          const int jj = SILU ? (j % TN) : j;
+          const int r = (SILU && j >= TN ? BN : 0) + wn * WTN + jj * 16 + (lane & 15);
+          bfr[j] = __builtin_bit_cast(bf16x8, *(const u32x4 *)&Bs[cur][r * LDS_STRIDE + col]);
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < NB; ++j) acc[i][j] = mfma_16x16x32(af[i], bfr[j], acc[i][j]);
+      }
+      if (kt + 1 < nk) store(cur ^ 1);
+      __syncthreads();
+    }
+
+    // Epilogue: lane holds rows (lane>>4)*4 + e of column lane&15 of each 16x16 tile.
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int n = n0 + wn * WTN + j * 16 + (lane & 15);
+        if (n >= p.N) continue;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int m = m0 + wm * WTM + i * 16 + (lane >> 4) * 4 + e;
+          if (m >= m_end) continue;
+          const float v = acc[i][j][e];
+          if (PARTIAL) {
+            const int64_t ncols = SILU ? 2 * (int64_t)p.N : p.N;
+            float *dst = p.partial + ((int64_t)split * p.M + m) * ncols;
+            dst[n] = v;
+            if (SILU) dst[p.N + n] = acc[i][TN + j][e];
+          } else if (EPI == EPI_BF16) {
+            ((uint16_t *)p.C)[(int64_t)m * p.ldc + n] = f2bf(v);
+          } else if (EPI == EPI_F32) {
+            ((float *)p.C)[(int64_t)m * p.ldc + n] = v;
+          } else if (EPI == EPI_RESID) {
+            uint16_t *c = (uint16_t *)p.C + (int64_t)m * p.ldc + n;
+            *c = f2bf(bf2f(*c) + v);
+          } else {  // SILU
+            const float up = acc[i][TN + j][e];
+            ((uint16_t *)p.C)[(int64_t)m * p.ldc + n] = f2bf(silu(v) * up);
+          }
+        }
+      }
+    }
+  }
+}
+
+// Sum split-K partials and apply the epilogue.
+template <int EPI>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs p) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total = (int64_t)p.M * p.N;
+  if (idx >= total) return;
+  const int m = (int)(idx / p.N), n = (int)(idx % p.N);
+  const int64_t ncols = EPI == EPI_SILU ? 2 * (int64_t)p.N : p.N;
+  float v = 0.f, up = 0.f;
+  for (int s = 0; s < p.splits; ++s) {
+    const float *row = p.partial + ((int64_t)s * p.M + m) * ncols;
+    v += row[n];
+    if (EPI == EPI_SILU) up += row[p.N + n];
+  }
+  if (EPI == EPI_BF16) {
+    ((uint16_t *)p.C)[(int64_t)m * p.ldc + n] = f2bf(v);
+  } else if (EPI == EPI_F32) {
+    ((float *)p.C)[(int64_t)m * p.ldc + n] = v;
+  } else if (EPI == EPI_RESID) {
+    uint16_t *c = (uint16_t *)p.C + (int64_t)m * p.ldc + n;
+    *c = f2bf(bf2f(*c) + v);
+  } else {
+    ((uint16_t *)p.C)[(int64_t)m * p.ldc + n] = f2bf(silu(v) * up);
+  }
+}
+
+constexpr int kBM = 64, kBN = 64;
+
+template <int EPI>
+hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
+  const int n_tiles = (a.N + kBN - 1) / kBN;
+  if (a.group_off) {
+    dim3 grid(n_tiles, 1, a.groups);
+    hipLaunchKernelGGL((gemm_kernel<kBM, kBN, 2, 2, EPI, false>), grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
+  const int m_tiles = (a.M + kBM - 1) / kBM;
+  if (a.splits > 1) {
+    dim3 grid(n_tiles, m_tiles, a.splits);
+    hipLaunchKernelGGL((gemm_kernel<kBM, kBN, 2, 2, EPI, true>), grid, dim3(256), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t total = (int64_t)a.M * a.N;
+    hipLaunchKernelGGL((splitk_reduce_kernel<EPI>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+                       s, a);
+    return hipGetLastError();
+  }
+  dim3 grid(n_tiles, m_tiles, 1);
+  hipLaunchKernelGGL((gemm_kernel<kBM, kBN, 2, 2, EPI, false>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int gemm_splits(int M, int N, int K, int epi) {
+  (void)epi;
+  const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+  const int steps = (K + BK - 1) / BK;
+  int s = 1;
+  // Narrow outputs leave most of the 256 compute units idle: split K until
+  // there are at least ~512 blocks, keeping >= 8 K steps per block.
+  while (tiles * s * 2 <= 512 && steps / (s * 2) >= 8) s *= 2;
+  return s;
+}
+
+size_t gemm_partial_bytes(int M, int N, int K, int epi) {
+  const int s = gemm_splits(M, N, K, epi);
+  if (s <= 1) return 0;
+  return (size_t)s * M * N * (epi == EPI_SILU ? 2 : 1) * sizeof(float);
+}
+
+hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  switch (a.epi) {
+    case EPI_BF16: return launch_epi<EPI_BF16>(a, s);
+    case EPI_F32: return launch_epi<EPI_F32>(a, s);
+    case EPI_RESID: return launch_epi<EPI_RESID>(a, s);
+    default: return launch_epi<EPI_SILU>(a, s);
+  }
+}
+
+}  // namespace ods

@@ -1,0 +1,210 @@
+// MoE routing and token permutation for the expert stage. In the paper's cost
+// model only the routed experts count toward the activated parameters while
+// every expert stays resident (Appendix A.4); these kernels turn per-token
+// routing into contiguous per-expert row groups for the grouped GEMMs and
+// scatter the expert outputs back. All integer outputs are deterministic.
+#include <math.h>
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace ods {
+
+namespace {
+
+// One wave per token: top-k of the fp32 logits (ties -> lower expert id), and
+// softmax over the chosen k. E <= 256 (four logits per lane), k <= 64.
+__global__ __launch_bounds__(256) void topk_kernel(const float *__restrict__ logits, int B, int E, int k,
+                                                   int32_t *__restrict__ ids, float *__restrict__ w) {
+  const int lane = threadIdx.x & 63;
+  const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (b >= B) return;
+  float v[4];
+  bool taken[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = lane + 64 * j;
+    v[j] = e < E ? logits[(int64_t)b * E + e] : -INFINITY;
+    taken[j] = e >= E;
+  }
+  float z0 = 0.f, sum = 0.f, my_z = 0.f;
+  int my_i = 0;
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = lane + 64 * j;
+      if (!taken[j] && (v[j] > bv || (v[j] == bv && e < bi))) {
+        bv = v[j];
+        bi = e;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, kWave);
+      const int oi = __shfl_xor(bi, o, kWave);
+      if (ov > bv || (ov == bv && oi < bi)) {
+        bv = ov;
+        bi = oi;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (lane + 64 * j == bi) taken[j] = true;
+    if (r == 0) z0 = bv;
+    sum += __expf(bv - z0);
+    if (lane == r) {
+      my_z = bv;
+      my_i = bi;
+    }
+  }
+  if (lane < k) {
+    ids[(int64_t)b * k + lane] = my_i;
+    w[(int64_t)b * k + lane] = __expf(my_z - z0) / sum;
+  }
+}
+
+// Single block, T threads, stable counting sort of the n = B*k (token, slot)
+// pairs by expert: thread t owns the contiguous pair segment [t*seg, (t+1)*seg)
+// and column t of a per-(expert, thread) count table; an exclusive scan of the
+// table in expert-major order gives every pair its sorted position.
+__global__ void permute_kernel(const int32_t *__restrict__ ids, int n, int E, int32_t *__restrict__ perm,
+                               int32_t *__restrict__ slot_pos, int32_t *__restrict__ expert_off) {
+  extern __shared__ uint32_t cnt[];  // [E][T] followed by T scan slots
+  const int T = blockDim.x, t = threadIdx.x;
+  uint32_t *tot = cnt + E * T;
+  const int seg = (n + T - 1) / T;
+  const int i0 = min(n, t * seg), i1 = min(n, i0 + seg);
+  for (int e = 0; e < E; ++e) cnt[e * T + t] = 0;
+  __syncthreads();
+  for (int i = i0; i < i1; ++i) {
+    const int e = ids[i];
+    if ((unsigned)e < (unsigned)E) cnt[e * T + t] += 1;
+  }
+  __syncthreads();
+  // exclusive scan over the flat table; thread t scans entries [t*E, (t+1)*E)
+  uint32_t local = 0;
+  for (int j = 0; j < E; ++j) local += cnt[t * E + j];
+  tot[t] = local;
+  __syncthreads();
+  if (t == 0) {
+    uint32_t run = 0;
+    for (int j = 0; j < T; ++j) {
+      const uint32_t x = tot[j];
+      tot[j] = run;
+      run += x;
+    }
+  }
+  __syncthreads();
+  uint32_t run = tot[t];
+  for (int j = 0; j < E; ++j) {
+    const uint32_t x = cnt[t * E + j];
+    cnt[t * E + j] = run;
+    run += x;
+  }
+  __syncthreads();
+  for (int e = t; e < E; e += T) expert_off[e] = (int32_t)cnt[e * T];
+  if (t == T - 1) expert_off[E] = (int32_t)run;
+  __syncthreads();  // the placement below advances the counters read above
+  for (int i = i0; i < i1; ++i) {
+    const int e = ids[i];
+    if ((unsigned)e < (unsigned)E) {
+      const uint32_t pos = cnt[e * T + t]++;
+      perm[pos] = i;
+      slot_pos[i] = (int32_t)pos;
+    } else {
+      slot_pos[i] = -1;
+    }
+  }
+}
+
+// dst[r] = src[perm[r] / k] for sorted rows r < expert_off[E]; rows past the end are zeroed.
+__global__ __launch_bounds__(256) void gather_rows_kernel(const uint16_t *__restrict__ src,
+                                                          const int32_t *__restrict__ perm, int k, int H,
+                                                          const int32_t *__restrict__ valid_rows,
+                                                          uint16_t *__restrict__ dst) {
+  const int r = blockIdx.x;
+  const int nvec = H / 8;
+  u32x4 *d = (u32x4 *)(dst + (int64_t)r * H);
+  if (r >= min((int)gridDim.x, *valid_rows)) {
+    for (int v = threadIdx.x; v < nvec; v += 256) d[v] = u32x4{0u, 0u, 0u, 0u};
+    return;
+  }
+  const int pr = perm[r];
+  if (pr < 0 || pr >= gridDim.x) {  // perm comes from device memory
+    for (int v = threadIdx.x; v < nvec; v += 256) d[v] = u32x4{0u, 0u, 0u, 0u};
+    return;
+  }
+  const u32x4 *s = (const u32x4 *)(src + (int64_t)(pr / k) * H);
+  for (int v = threadIdx.x; v < nvec; v += 256) d[v] = s[v];
+}
+
+// resid[b] = bf16(resid[b] + sum_j w[b, j] * yp[slot_pos[b*k + j]]), fp32 accumulation.
+__global__ __launch_bounds__(256) void moe_combine_kernel(const uint16_t *__restrict__ yp,
+                                                          const float *__restrict__ w,
+                                                          const int32_t *__restrict__ slot_pos, int k, int H,
+                                                          int n_rows, uint16_t *__restrict__ resid) {
+  const int b = blockIdx.x;
+  const int nvec = H / 8;
+  u32x4 *r = (u32x4 *)(resid + (int64_t)b * H);
+  for (int v = threadIdx.x; v < nvec; v += 256) {
+    float acc[8];
+    const u32x4 x = r[v];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      acc[2 * j] = 0.f;
+      acc[2 * j + 1] = 0.f;
+    }
+    for (int j = 0; j < k; ++j) {
+      const int pos = slot_pos[(int64_t)b * k + j];
+      if (pos < 0 || pos >= n_rows) continue;
+      const float wj = w[(int64_t)b * k + j];
+      const u32x4 y = *((const u32x4 *)(yp + (int64_t)pos * H) + v);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc[2 * q] += wj * bf_lo(y[q]);
+        acc[2 * q + 1] += wj * bf_hi(y[q]);
+      }
+    }
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = pack2(bf_lo(x[q]) + acc[2 * q], bf_hi(x[q]) + acc[2 * q + 1]);
+    r[v] = o;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_topk(const float *logits, int B, int E, int k, int32_t *ids, float *w, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(topk_kernel, dim3((B + 3) / 4), dim3(256), 0, s, logits, B, E, k, ids, w);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute(const int32_t *ids, int B, int k, int E, int32_t *perm, int32_t *slot_pos,
+                          int32_t *expert_off, hipStream_t s) {
+  const int n = B * k;
+  // Count table [E][T] of 32-bit counters plus T scan slots, within 64 KiB of LDS.
+  int T = 256;
+  while (T > 16 && ((size_t)E * T + T) * 4 > 65536) T /= 2;
+  const size_t lds = ((size_t)E * T + T) * sizeof(uint32_t);
+  hipLaunchKernelGGL(permute_kernel, dim3(1), dim3(T), lds, s, ids, n, E, perm, slot_pos, expert_off);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(const uint16_t *src, const int32_t *perm, const int32_t *valid_rows,
+                                  int rows, int k, int H, uint16_t *dst, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(rows), dim3(256), 0, s, src, perm, k, H, valid_rows, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_moe_combine(const uint16_t *yp, const float *w, const int32_t *slot_pos, int B, int k,
+                              int H, uint16_t *resid, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(moe_combine_kernel, dim3(B), dim3(256), 0, s, yp, w, slot_pos, k, H, B * k, resid);
+  return hipGetLastError();
+}
+
+}  // namespace ods

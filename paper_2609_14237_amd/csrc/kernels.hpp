@@ -1,0 +1,65 @@
+// Internal launch interface between the host dispatcher and the gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ods {
+
+enum Epilogue : int {
+  EPI_BF16 = 0,   // C = bf16(acc)
+  EPI_F32 = 1,    // C = acc (fp32 output)
+  EPI_RESID = 2,  // C = bf16(C + acc), C is the residual stream (in place)
+  EPI_SILU = 3,   // C[:, n] = bf16(silu(acc_gate) * acc_up), B rows n (gate) and n_up + n (up)
+};
+
+// C[m, n] = sum_k A[m, k] * B[n, k] with an epilogue. A, B, C row-major.
+struct GemmArgs {
+  const uint16_t *A; int64_t lda;
+  const uint16_t *B; int64_t ldb; int64_t b_group_stride;
+  void *C; int64_t ldc;
+  int M, N, K;
+  int n_up;                   // EPI_SILU: row offset of the "up" half inside B
+  int epi;
+  const int32_t *group_off;   // grouped GEMM: rows [off[g], off[g+1]) use B + g * b_group_stride
+  int groups;
+  int splits;                 // split-K count (>1: fp32 partials in `partial`, then a reduce)
+  float *partial;
+};
+
+// Split-K plan for a dense GEMM (shared by sizing and launching).
+int gemm_splits(int M, int N, int K, int epi);
+size_t gemm_partial_bytes(int M, int N, int K, int epi);
+hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
+
+hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gain, uint16_t *out, int rows, int H,
+                          float eps, hipStream_t s);
+
+// In-place RoPE of the q and k heads of qkv and/or append of k, v to the KV pool.
+hipError_t launch_rope_append(uint16_t *qkv, int B, int n_q, int n_kv, int D, float theta,
+                              const int32_t *ctx_lens, const int32_t *page_table, int max_pages,
+                              uint16_t *pool, int64_t pool_pages, bool do_rope, bool do_append,
+                              hipStream_t s);
+
+// Paged GQA decode attention (split over pages) + exact log-sum-exp merge.
+struct AttnPlan {
+  int split_pages;  // pages per work item
+  int n_splits;     // work items per (sequence, kv head)
+};
+AttnPlan attn_plan(int B, int n_kv, int D, int max_pages, int window, int split_pages_req);
+size_t attn_ws_bytes(int B, int n_q, int D, const AttnPlan &plan);
+hipError_t launch_attention(const uint16_t *qkv, int B, int n_q, int n_kv, int D, int window,
+                            const int32_t *ctx_lens, const int32_t *page_table, int max_pages,
+                            const uint16_t *pool, int64_t pool_pages, const AttnPlan &plan,
+                            float *ws, uint16_t *o, hipStream_t s);
+
+hipError_t launch_silu_mul(const uint16_t *gu, uint16_t *act, int rows, int F, hipStream_t s);
+
+hipError_t launch_topk(const float *logits, int B, int E, int k, int32_t *ids, float *w, hipStream_t s);
+hipError_t launch_permute(const int32_t *ids, int B, int k, int E, int32_t *perm, int32_t *slot_pos,
+                          int32_t *expert_off, hipStream_t s);
+hipError_t launch_gather_rows(const uint16_t *src, const int32_t *perm, const int32_t *valid_rows,
+                              int rows, int k, int H, uint16_t *dst, hipStream_t s);
+hipError_t launch_moe_combine(const uint16_t *yp, const float *w, const int32_t *slot_pos, int B,
+                              int k, int H, uint16_t *resid, hipStream_t s);
+
+}  // namespace ods

@@ -1,0 +1,122 @@
+"""PyTorch-side marshalling around the C ABI: packs device tensors into the
+ods_* structs and allocates the live buffers and workspace the library sizes.
+No operator of the decode step is computed here."""
+from __future__ import annotations
+
+import ctypes as C
+
+import torch
+
+from . import binding as _b
+from .binding import ods_batch, ods_block, ods_layer, ods_layer_cfg, ods_state
+
+
+def layer_cfg(cfg) -> ods_layer_cfg:
+    """ods_layer_cfg from any object with the layer-shape attributes."""
+    return ods_layer_cfg(cfg.hidden, cfg.n_q, cfg.n_kv, cfg.head_dim, cfg.ffn, cfg.n_experts, cfg.top_k,
+                         cfg.moe_ffn, cfg.window, cfg.rope_theta, cfg.rms_eps)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return t.data_ptr()
+
+
+class DeviceBlock:
+    """ods_block over per-layer weight dicts and KV pools (tensors stay referenced)."""
+
+    def __init__(self, cfgs, weights, pools, pool_pages: int):
+        self.cfgs = list(cfgs)
+        self.weights = list(weights)
+        self.pools = list(pools)
+        n = len(self.cfgs)
+        self._layers = (ods_layer * n)()
+        for i, (cfg, w, pool) in enumerate(zip(self.cfgs, self.weights, self.pools)):
+            L = self._layers[i]
+            L.cfg = layer_cfg(cfg)
+            for name in ("g_attn", "w_qkv", "w_o", "g_ffn", "w_gate_up", "w_down", "w_router"):
+                setattr(L, name, _ptr(w.get(name)))
+            L.kv_pool = _ptr(pool)
+            L.pool_pages = pool_pages if pool is not None else 0
+        self.c = ods_block(n, C.cast(self._layers, C.POINTER(ods_layer)))
+
+    def num_ops(self) -> int:
+        return _b.ods_block_num_ops(self.c)
+
+    def op_name(self, op: int):
+        return _b.ods_op_name(self.c, op)
+
+    def layer_offset(self, layer: int) -> int:
+        return sum(14 if c.n_experts else 10 for c in self.cfgs[:layer])
+
+
+class DeviceBatch:
+    """ods_batch over device int32 ctx_lens [B] and page_table [B, max_pages]."""
+
+    def __init__(self, ctx_lens: torch.Tensor, page_table: torch.Tensor, split_pages: int = 0):
+        assert ctx_lens.dtype == torch.int32 and page_table.dtype == torch.int32
+        self.ctx_lens = ctx_lens.contiguous()
+        self.page_table = page_table.contiguous()
+        B, max_pages = self.page_table.shape
+        self.c = ods_batch(B, max_pages, _ptr(self.ctx_lens), _ptr(self.page_table), split_pages)
+
+    @property
+    def batch(self) -> int:
+        return self.c.batch
+
+
+_BUF_DTYPE = {"logits": torch.float32, "topk_w": torch.float32, "topk_ids": torch.int32,
+              "perm": torch.int32, "slot_pos": torch.int32, "expert_off": torch.int32}
+
+
+class DeviceState:
+    """Live buffers sized by ods_live_bytes and a workspace of ods_workspace_bytes."""
+
+    def __init__(self, block: DeviceBlock, batch: DeviceBatch, device="cuda", fill=None):
+        self.buffers = {}
+        for i, name in enumerate(_b.BUFFERS):
+            nbytes = _b.ods_live_bytes(block.c, batch.batch, i)
+            if nbytes == 0:
+                continue
+            dt = _BUF_DTYPE.get(name, torch.bfloat16)
+            n = nbytes // torch.tensor([], dtype=dt).element_size()
+            t = torch.empty(n, dtype=dt, device=device)
+            if fill is not None:
+                t.fill_(fill if dt != torch.int32 else -7)
+            self.buffers[name] = t
+        self.ws_bytes = _b.ods_workspace_bytes(block.c, batch.c)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        self.c = ods_state()
+        for name, t in self.buffers.items():
+            setattr(self.c, name, t.data_ptr())
+        self.c.ws = self.ws.data_ptr()
+        self.c.ws_bytes = self.ws_bytes
+
+    def view(self, name: str, *shape):
+        t = self.buffers[name]
+        n = 1
+        for s in shape:
+            n *= s
+        return t[:n].view(*shape)
+
+
+def current_stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def run_partition(block: DeviceBlock, op_begin: int, op_end: int, batch: DeviceBatch, state: DeviceState,
+                  stream: int | None = None) -> None:
+    st = _b.ods_run_partition(block.c, op_begin, op_end, batch.c, state.c,
+                              current_stream() if stream is None else stream)
+    _b._check(st, f"ods_run_partition[{op_begin},{op_end})")
+
+
+def attn_stage(block, layer, batch, state, stream=None) -> None:
+    st = _b.ods_attn_stage(block.c, layer, batch.c, state.c, current_stream() if stream is None else stream)
+    _b._check(st, f"ods_attn_stage({layer})")
+
+
+def ffn_stage(block, layer, batch, state, stream=None) -> None:
+    st = _b.ods_ffn_stage(block.c, layer, batch.c, state.c, current_stream() if stream is None else stream)
+    _b._check(st, f"ods_ffn_stage({layer})")

@@ -1,0 +1,151 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads and exports
+every symbol the header declares, the page allocator agrees bit-for-bit with
+the oracle's independent implementation, buffer sizing, and every argument
+error path (all of which return before anything is enqueued)."""
+import ctypes as C
+import os
+import re
+from dataclasses import replace
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from workloads import gen
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+B = pytest.importorskip("paper_2609_14237_amd.binding")
+from paper_2609_14237_amd import runtime as R  # noqa: E402
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "ods.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ods_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = header_functions()
+    assert len(names) >= 10
+    lib = C.CDLL(B.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(B.SIGNATURES)
+
+
+@pytest.mark.parametrize("w", W.ALL, ids=lambda w: w.name)
+def test_kv_alloc_matches_oracle_bit_exactly(w):
+    ctx = gen.contexts(w)
+    P = gen.pool_pages_for(ctx)
+    table = np.zeros((w.batch, w.max_pages), dtype=np.int32)
+    assert B.ods_kv_alloc(P, ctx, w.batch, w.seed, w.max_pages, table) == B.ODS_OK
+    np.testing.assert_array_equal(table, O.kv_alloc(ctx, P, w.seed, w.max_pages))
+
+
+def test_kv_alloc_small_vector_and_errors():
+    ctx = np.array([20, 16, 1, 33], dtype=np.int32)
+    t = np.zeros((4, 3), dtype=np.int32)
+    assert B.ods_kv_alloc(10, ctx, 4, 0, 3, t) == B.ODS_OK
+    np.testing.assert_array_equal(t, O.kv_alloc(ctx, 10, 0, 3))
+    assert B.ods_kv_alloc(5, ctx, 4, 0, 3, t) == B.ODS_ENOMEM
+    assert B.ods_kv_alloc(10, ctx, 4, 0, 2, t) == B.ODS_ERANGE
+    bad = np.array([20, 0], dtype=np.int32)
+    assert B.ods_kv_alloc(10, bad, 2, 0, 3, t) == B.ODS_EINVAL
+    assert B.lib.ods_kv_alloc(10, None, 4, 0, 3, t.ctypes.data_as(C.POINTER(C.c_int32))) == B.ODS_EINVAL
+    assert "pool" in B.ods_last_error() or "null" in B.ods_last_error()
+
+
+FAKE = 0x10000  # an aligned, never-dereferenced address: every call below fails validation first
+
+
+def fake_block(cfgs):
+    ws = [{k: FAKE_T for k in ("g_attn", "w_qkv", "w_o", "g_ffn", "w_gate_up", "w_down", "w_router")}
+          for _ in cfgs]
+    return R.DeviceBlock(cfgs, ws, [FAKE_T] * len(cfgs), 100)
+
+
+class _FakeTensor:
+    def data_ptr(self):
+        return FAKE
+
+
+FAKE_T = _FakeTensor()
+
+
+def fake_state(**override):
+    s = B.ods_state()
+    for name in B.BUFFERS:
+        setattr(s, name, FAKE)
+    s.ws = FAKE
+    s.ws_bytes = 1 << 40
+    for k, v in override.items():
+        setattr(s, k, v)
+    return s
+
+
+def fake_batch(batch=4, max_pages=8):
+    return B.ods_batch(batch, max_pages, FAKE, FAKE, 0)
+
+
+def test_block_ops_and_names():
+    blk = fake_block(W.HYBRID_4L.layers)
+    assert blk.num_ops() == 40
+    assert blk.op_name(4) == "attn_core" and blk.op_name(39) == "down_residual"
+    assert blk.op_name(40) is None
+    moe = fake_block(W.MOE_B512.layers)
+    assert moe.num_ops() == 14
+    assert [moe.op_name(i) for i in range(7, 14)] == ["router", "topk_softmax", "moe_permute", "expert_gate_up",
+                                                      "silu_mul", "expert_down", "moe_combine_residual"]
+
+
+@pytest.mark.parametrize("rng", [(-1, 3), (0, 0), (5, 4), (0, 11), (10, 11)])
+def test_range_errors(rng):
+    blk = fake_block(W.TINY.layers)
+    st = B.ods_run_partition(blk.c, rng[0], rng[1], fake_batch(), fake_state(), 0)
+    assert st == B.ODS_ERANGE
+
+
+@pytest.mark.parametrize("buf,op", [("xn", (0, 1)), ("qkv", (1, 2)), ("o", (4, 5)), ("resid", (5, 6)),
+                                    ("hn", (6, 7)), ("act", (7, 9)), ("gu", (7, 8)), ("ws", (4, 5))])
+def test_null_live_buffer_is_rejected(buf, op):
+    blk = fake_block(W.TINY.layers)
+    st = B.ods_run_partition(blk.c, op[0], op[1], fake_batch(), fake_state(**{buf: None}), 0)
+    assert st == B.ODS_EINVAL
+    assert buf in B.ods_last_error()
+
+
+def test_misaligned_pointer_is_rejected():
+    blk = fake_block(W.TINY.layers)
+    st = B.ods_run_partition(blk.c, 0, 1, fake_batch(), fake_state(xn=FAKE + 2), 0)
+    assert st == B.ODS_EINVAL and "aligned" in B.ods_last_error()
+
+
+def test_unsupported_shapes():
+    for cfg in (replace(W.TINY.layers[0], head_dim=96), replace(W.TINY.layers[0], n_q=5),
+                replace(W.TINY.layers[0], n_q=64, n_kv=2), replace(W.TINY.layers[0], ffn=690),
+                replace(W.MOE_B512.layers[0], top_k=65, n_experts=128)):
+        blk = fake_block([cfg])
+        assert B.ods_run_partition(blk.c, 0, 1, fake_batch(), fake_state(), 0) == B.ODS_EUNSUPPORTED
+
+
+def test_workspace_too_small():
+    blk = fake_block(W.DENSE_8B_B64.layers)
+    batch = fake_batch(64, 256)
+    need = B.ods_workspace_bytes(blk.c, batch)
+    assert need > 0
+    st = B.ods_run_partition(blk.c, 4, 5, batch, fake_state(ws_bytes=need - 1), 0)
+    assert st == B.ODS_ENOMEM
+
+
+def test_buffer_sizes():
+    blk = fake_block(W.MOE_B512.layers)
+    n = 512
+    assert B.ods_live_bytes(blk.c, n, B.BUFFERS.index("resid")) == n * 4096 * 2
+    assert B.ods_live_bytes(blk.c, n, B.BUFFERS.index("qkv")) == n * (32 + 8) * 128 * 2
+    assert B.ods_live_bytes(blk.c, n, B.BUFFERS.index("xp")) == n * 8 * 4096 * 2
+    assert B.ods_live_bytes(blk.c, n, B.BUFFERS.index("expert_off")) == 65 * 4
+    assert B.ods_live_bytes(blk.c, n, B.BUFFERS.index("gu")) == 0
+    cfg = R.layer_cfg(W.DENSE_8B_B64.layers[0])
+    assert B.ods_kv_pool_bytes(cfg, 10) == 10 * 2 * 8 * 16 * 128 * 2
