@@ -1,0 +1,295 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark of the ODS hot path on one MI355X.
+
+One step = one decode step of the workload's block (for the default workload,
+one 8B-shaped dense layer: the attention stage, ops [0, 6), then the FFN stage,
+ops [6, 10)) over the whole batch, with every input already resident in HBM.
+Three independent copies of the weights and KV pools are used in rotation so
+that no step finds the previous step's bytes in the 256 MB last-level cache.
+
+Prints one JSON line: whole-step decode tokens/s, per-stage tokens/s with their
+fraction of the HBM / MFMA roofline, the roofline of the dominant operator
+(attn_core) timed with HIP events inside the timed loop, and the CPU oracle
+timed on the host on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12          # bytes/s, MI355X HBM3E
+MFMA_BF16_PEAK = 2.5e15    # dense bf16 flop/s, MI355X
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_core_traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="dense8b_b64")
+    ap.add_argument("--copies", type=int, default=0, help="weight/KV copies in rotation (0: auto)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work to time")
+    return ap.parse_args()
+
+
+# ----------------------------------------------------------------------------- accounting
+
+def layer_accounting(cfg, ctx, B):
+    """Algorithmic bytes / flops per stage of one layer (what the method must
+    move or compute; intermediates excluded)."""
+    H, nq, nkv, d = cfg.hidden, cfg.n_q, cfg.n_kv, cfg.head_dim
+    pos = ctx.astype(np.int64) - 1
+    if cfg.window > 0:
+        leff = np.minimum(ctx, cfg.window).astype(np.int64)
+    else:
+        leff = ctx.astype(np.int64)
+    kv_bytes = int(leff.sum()) * 2 * nkv * d * 2
+    w_attn = (cfg.qkv_dim * H + H * nq * d) * 2
+    attn_core_bytes = kv_bytes + 2 * B * nq * d * 2
+    attn_bytes = kv_bytes + w_attn + 4 * B * H + 4 * B * nkv * d
+    attn_flops = 2 * B * H * cfg.qkv_dim + 2 * B * nq * d * H + 4 * nq * d * int(leff.sum())
+    if cfg.n_experts:
+        E, k, I = cfg.n_experts, cfg.top_k, cfg.moe_ffn
+        ffn_bytes = 6 * H * I * E + 2 * H * E + 4 * B * H
+        ffn_flops = 6 * B * k * H * I + 2 * B * H * E
+    else:
+        F = cfg.ffn
+        ffn_bytes = 6 * H * F + 4 * B * H
+        ffn_flops = 6 * B * H * F
+    del pos
+    return dict(attn_bytes=attn_bytes, attn_flops=attn_flops, attn_core_bytes=attn_core_bytes,
+                kv_bytes=kv_bytes, ffn_bytes=ffn_bytes, ffn_flops=ffn_flops)
+
+
+def attn_source_hash():
+    h = hashlib.sha256()
+    for f in ("k_attn.hip", "common.hpp"):
+        with open(os.path.join(ROOT, "paper_2609_14237_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload):
+    """HBM bytes per attn_core launch from the committed rocprofv3 counter
+    summary, only if it was taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    rec = t.get(workload)
+    if not rec or rec.get("source_hash") != attn_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+# ----------------------------------------------------------------------------- CPU baseline
+
+def cpu_baseline(w, copy0, budget_s):
+    """Time the float64 oracle on the host over whole-batch decode steps of the
+    same workload (first weight/KV copy), repeated until ~budget_s."""
+    import oracle as O
+    import torch
+    from threadpoolctl import threadpool_info
+
+    def f64(t):
+        return t.detach().float().cpu().numpy().astype(np.float64)
+
+    cfgs = list(w.layers)
+    n_rows = w.batch
+    rows = np.arange(n_rows)
+    # inputs of the sampled rows (their pages only), converted once, not timed
+    ctx = copy0["ctx"][rows]
+    pt = copy0["page_table"][rows]
+    n_pages = [-(-int(c) // 16) for c in ctx]
+    pages = np.concatenate([pt[i, :n] for i, n in enumerate(n_pages)])
+    sub = np.full((len(rows), pt.shape[1]), -1, dtype=np.int32)
+    off = 0
+    for i, n in enumerate(n_pages):
+        sub[i, :n] = np.arange(off, off + n)
+        off += n
+    idx = torch.from_numpy(pages.astype(np.int64)).cuda()
+    weights = [{k: f64(v) for k, v in wl.items()} for wl in copy0["weights"]]
+    pools0 = [f64(p.index_select(0, idx)) for p in copy0["pools"]]
+    x = f64(copy0["x"][torch.from_numpy(rows).cuda()])
+    n_ops = sum(14 if c.n_experts else 10 for c in cfgs)
+    done, t_total, reps = 0, 0.0, 0
+    while True:
+        pools = [p.copy() for p in pools0]
+        t0 = time.perf_counter()
+        O.run_ops(cfgs, weights, pools, sub, ctx, {"resid": x.copy()}, 0, n_ops)
+        t_total += time.perf_counter() - t0
+        done += len(rows)
+        reps += 1
+        if t_total >= budget_s * 0.5 or reps >= 50:
+            break
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": done / t_total, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{reps} whole-batch decode steps ({len(rows)} sequences, all ops) of the "
+                      f"{w.name} workload, float64 numpy oracle, {t_total:.1f} s"}
+
+
+# ----------------------------------------------------------------------------- main
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(collectives and sharding are out of scope); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    from workloads import gen
+    from paper_2609_14237_amd import binding as B
+    from paper_2609_14237_amd import runtime as R
+
+    w = W.BY_NAME[args.workload]
+    dev = "cuda"
+    torch.cuda.set_device(0)
+    ctx = gen.contexts(w)
+    P = gen.pool_pages_for(ctx)
+    max_pages = w.max_pages
+    page_table = np.zeros((w.batch, max_pages), dtype=np.int32)
+    assert B.ods_kv_alloc(P, ctx, w.batch, w.seed, max_pages, page_table) == 0, B.ods_last_error()
+
+    # per-step working set decides how many rotated copies are needed to defeat the 256 MB MALL
+    acct = [layer_accounting(c, ctx, w.batch) for c in w.layers]
+    step_bytes = sum(a["attn_bytes"] + a["ffn_bytes"] for a in acct)
+    copies = args.copies or (3 if step_bytes < 2e9 else 1)
+
+    batch = R.DeviceBatch(torch.from_numpy(ctx).to(dev), torch.from_numpy(page_table).to(dev))
+    sets = []
+    for c in range(copies):
+        seed = w.seed + 1000 * c
+        weights = [{k: v for k, v in gen.layer_weights(cfg, seed, l, dev, w.router_std).items()}
+                   for l, cfg in enumerate(w.layers)]
+        pools = [gen.kv_pool(cfg, P, seed, l, dev) for l, cfg in enumerate(w.layers)]
+        x = gen.activations(w.batch, w.layers[0].hidden, seed, dev)
+        blk = R.DeviceBlock(w.layers, weights, pools, P)
+        state = R.DeviceState(blk, batch, dev)
+        sets.append(dict(block=blk, state=state, weights=weights, pools=pools, x=x, ctx=ctx,
+                         page_table=page_table))
+    torch.cuda.synchronize()
+
+    # stage boundaries: each layer as [0,4) [4,5) [5,6) | [6,N) -- the cut around attn_core
+    # changes no kernel (no fusion crosses it) and lets events time that operator alone
+    n_layers = len(w.layers)
+    offs = [sets[0]["block"].layer_offset(l) for l in range(n_layers)]
+    ends = [offs[l] + (14 if w.layers[l].n_experts else 10) for l in range(n_layers)]
+    stream = torch.cuda.current_stream()
+    sptr = stream.cuda_stream
+
+    def run_step(s, evs=None):
+        blk, st = s["block"].c, s["state"].c
+        for l in range(n_layers):
+            o = offs[l]
+            for a, b, tag in ((o, o + 4, None), (o + 4, o + 5, "core"), (o + 5, o + 6, "attn"),
+                              (o + 6, ends[l], "ffn")):
+                rc = B.ods_run_partition(blk, a, b, batch.c, st, sptr)
+                if rc != 0:
+                    raise B.OdsError(rc, f"ods_run_partition[{a},{b})")
+                if evs is not None:
+                    evs.append((l, tag, torch.cuda.Event(enable_timing=True)))
+                    evs[-1][2].record(stream)
+
+    for s in sets:
+        s["state"].view("resid", w.batch, w.layers[0].hidden).copy_(s["x"])
+    for i in range(args.warmup):
+        run_step(sets[i % copies])
+    torch.cuda.synchronize()
+
+    per_step_events = []
+    t_begin = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_begin.record(stream)
+    for i in range(args.steps):
+        evs = []
+        start = torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        run_step(sets[i % copies], evs)
+        per_step_events.append((start, evs))
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_begin.elapsed_time(t_end)
+    ms_per_step = total_ms / args.steps
+
+    # per-stage and attn_core durations from the in-loop events
+    core_ms, attn_ms, ffn_ms = [], [], []
+    for start, evs in per_step_events:
+        prev = start
+        a_ms = f_ms = c_ms = 0.0
+        layer_start = start
+        for (l, tag, ev) in evs:
+            dt = prev.elapsed_time(ev)
+            if tag == "core":
+                c_ms += dt
+            if tag == "attn":
+                a_ms += layer_start.elapsed_time(ev)
+            if tag == "ffn":
+                f_ms += dt
+                layer_start = ev
+            prev = ev
+        core_ms.append(c_ms)
+        attn_ms.append(a_ms)
+        ffn_ms.append(f_ms)
+    t_core = float(np.median(core_ms)) * 1e-3 / n_layers
+    t_attn = float(np.median(attn_ms)) * 1e-3
+    t_ffn = float(np.median(ffn_ms)) * 1e-3
+    attn_bytes = sum(a["attn_bytes"] for a in acct)
+    attn_flops = sum(a["attn_flops"] for a in acct)
+    ffn_bytes = sum(a["ffn_bytes"] for a in acct)
+    ffn_flops = sum(a["ffn_flops"] for a in acct)
+    core_bytes = sum(a["attn_core_bytes"] for a in acct) / n_layers
+
+    def stage(t, nbytes, flops):
+        return {"tokens_per_s": w.batch / t, "us": t * 1e6,
+                "hbm_GBps": nbytes / t / 1e9, "hbm_frac": nbytes / t / HBM_PEAK,
+                "mfma_TFLOPs": flops / t / 1e12, "mfma_frac": flops / t / MFMA_BF16_PEAK,
+                "roofline_us": max(nbytes / HBM_PEAK, flops / MFMA_BF16_PEAK) * 1e6}
+
+    achieved = core_bytes / t_core
+    traffic = measured_traffic(w.name)
+    result = {
+        "metric": "decode tokens/s per stage (attn, FFN) at 8B-shape layer; % HBM / MFMA peak",
+        "value": w.batch * args.steps / (total_ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "description": w.description, "batch": w.batch,
+                   "ctx_range": [w.ctx_lo, w.ctx_hi], "ctx_mean": float(ctx.mean()),
+                   "layers": n_layers, "copies_rotated": copies,
+                   "step": "attention stage [0,6) then FFN stage [6,N) per layer"},
+        "stages": {"attn": stage(t_attn, attn_bytes, attn_flops), "ffn": stage(t_ffn, ffn_bytes, ffn_flops)},
+        "roofline": {"kernel": "attn_core (split-K paged decode attention + LSE merge)",
+                     "bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK,
+                     "traffic": traffic,
+                     "algorithmic_bytes_per_launch": core_bytes, "avg_launch_us": t_core * 1e6},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, sets[0], args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
