@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--copies", type=int, default=0, help="weight/KV copies in rotation (0: auto)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work to time")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="before the timed loop, run one plain device copy of this many MiB (a known-size "
+                         "reference for hardware byte counters)")
     return ap.parse_args()
 
 
@@ -204,6 +207,14 @@ def main():
                     evs.append((l, tag, torch.cuda.Event(enable_timing=True)))
                     evs[-1][2].record(stream)
 
+    if args.calib_copy_mib:
+        src = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for s in sets:
         s["state"].view("resid", w.batch, w.layers[0].hidden).copy_(s["x"])
     for i in range(args.warmup):

@@ -2,19 +2,25 @@
 //
 // Decode attention is the memory-bound operator class of the paper's cost
 // model (Appendix A.2): each decoded token reads its whole KV context once.
-// Work item = one wave = (sequence b, KV head g, a run of `split_pages` pages).
-// All n_q / n_kv query heads of the group share the item, so every K/V byte is
-// read from HBM exactly once. Per page (16 tokens):
-//   S^T = K_page * Q_g^T    4 x MFMA 16x16x32 (d = 128): rows = tokens, cols = heads;
+//
+// Work item = one workgroup of 4 waves = (sequence b, KV head g, a chunk of
+// `chunk_pages` consecutive pages of the attended window); the waves take the
+// chunk's pages round-robin. All n_q / n_kv query heads of the group share the
+// item, so every K/V byte is read from HBM exactly once. Per page (16 tokens):
+//   S^T = K_page * Q_g^T    MFMA 16x16x32 (D/32 of them): rows = tokens, cols = heads;
 //                           lane l gets tokens (l/16)*4 .. +3 of head l%16.
 //   online softmax          per lane (head l%16); page max over the 4 lane rows
 //                           by two xor-shuffles; masked tokens get -inf.
-//   O^T += V_page^T * P     8 x MFMA 16x16x16 (d = 128): V is stored dim-major in
+//   O^T += V_page^T * P     MFMA 16x16x16 (D/16 of them): V is stored dim-major in
 //                           the page, so lane l reads 8 contiguous bytes, and P
 //                           is already in the B-operand layout of S^T.
 // The accumulator O^T keeps head l%16 in lane l, so the softmax rescale never
-// leaves the lane. Partials (m, l, acc[d]) go to a workspace and a second
-// kernel merges the splits exactly with their log-sum-exp weights.
+// leaves the lane. The 4 waves merge their (m, l, acc) through LDS; a sequence
+// whose window fits in one chunk writes o directly, longer ones write one
+// partial per chunk and a second kernel merges the chunks with their
+// log-sum-exp weights. K/V registers are reloaded as soon as the MFMA that
+// reads them has issued, so a wave keeps one page in flight with ~100 VGPRs
+// and four waves fit per SIMD.
 #include <math.h>
 
 #include <algorithm>
@@ -27,20 +33,22 @@ namespace ods {
 namespace {
 
 template <int D>
-__global__ __launch_bounds__(256) void attn_split_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) void attn_chunk_kernel(
     const uint16_t *__restrict__ qkv, int n_q, int n_kv, int window, const int32_t *__restrict__ ctx_lens,
     const int32_t *__restrict__ page_table, int max_pages, const uint16_t *__restrict__ pool,
-    int64_t pool_pages, int split_pages, int n_splits, float scale_log2, float *__restrict__ ws_acc,
-    float *__restrict__ ws_ml, int B) {
+    int64_t pool_pages, int chunk_pages, int n_chunks, float scale_log2, float *__restrict__ ws_acc,
+    float *__restrict__ ws_ml, uint16_t *__restrict__ o, int B) {
   constexpr int KK = D / 32;  // QK MFMAs per page
   constexpr int NB = D / 16;  // PV MFMAs per page
   constexpr int64_t BLK = (int64_t)kPage * D;
+  __shared__ float s_acc[3][NB * 4][64];  // waves 1..3, [register][lane]: conflict-free
+  __shared__ float s_m[4][16], s_l[4][16];
 
-  const int lane = threadIdx.x & 63;
-  const int gw = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int split = gw % n_splits;
-  const int g = (gw / n_splits) % n_kv;
-  const int b = gw / (n_splits * n_kv);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int item = blockIdx.x;
+  const int chunk = item % n_chunks;
+  const int g = (item / n_chunks) % n_kv;
+  const int b = item / (n_chunks * n_kv);
   if (b >= B) return;
   const int group = n_q / n_kv;
   const int ctx = min(ctx_lens[b], max_pages * kPage);
@@ -48,12 +56,13 @@ __global__ __launch_bounds__(256) void attn_split_kernel(
   const int p = ctx - 1;
   const int lo = window > 0 ? max(0, p - window + 1) : 0;
   const int first_page = lo / kPage, last_page = p / kPage;
-  const int pg_begin = first_page + split * split_pages;
-  if (pg_begin > last_page) return;
-  const int pg_end = min(pg_begin + split_pages, last_page + 1);
+  const int pg_begin = first_page + chunk * chunk_pages;
+  if (pg_begin > last_page) return;  // uniform over the block
+  const int pg_end = min(pg_begin + chunk_pages, last_page + 1);
+  const int chunks_b = (last_page - first_page + chunk_pages) / chunk_pages;
 
-  const int hl = lane & 15;   // head within the group (MFMA column)
-  const int rq = lane >> 4;   // lane row-quad
+  const int hl = lane & 15;  // head within the group (MFMA column)
+  const int rq = lane >> 4;  // lane row-quad
   const bool head_ok = hl < group;
 
   bf16x8 qf[KK];
@@ -75,134 +84,196 @@ __global__ __launch_bounds__(256) void attn_split_kernel(
   const uint16_t *pool_g = pool + (int64_t)g * BLK;
   const int64_t page_stride = 2 * (int64_t)n_kv * BLK;
   const int64_t v_off = (int64_t)n_kv * BLK;
-
-  // Page ids of this work item, one per lane (split_pages <= 64), broadcast
-  // with readlane so the K/V loads never wait on a dependent scalar load.
+  // Page ids of the chunk, one per lane (chunk_pages <= 64), broadcast with
+  // readlane so the K/V loads never wait on a dependent scalar load.
   const int my_page = (lane < pg_end - pg_begin) ? pt[pg_begin + lane] : -1;
+  auto page_ptr = [&](int pg, bool &ok) {
+    int page = __builtin_amdgcn_readlane(my_page, pg - pg_begin);
+    ok = (unsigned)page < (unsigned long long)pool_pages;
+    return pool_g + (int64_t)(ok ? page : 0) * page_stride;
+  };
 
   u32x4 kf[KK];
   u32x2 vf[NB];
-  auto fetch = [&](int pg, bool &ok) {
-    int page = __builtin_amdgcn_readlane(my_page, pg - pg_begin);
-    ok = (unsigned)page < (unsigned long long)pool_pages;
-    if (!ok) page = 0;
-    const uint16_t *kb = pool_g + (int64_t)page * page_stride;
-    const uint16_t *vb = kb + v_off;
+  int pg = pg_begin + wave;
+  bool ok = false;
+  if (pg < pg_end) {
+    const uint16_t *kb = page_ptr(pg, ok);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) kf[kk] = *(const u32x4 *)(kb + hl * D + kk * 32 + rq * 8);
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) vf[nb] = *(const u32x2 *)(vb + (nb * 16 + hl) * kPage + rq * 4);
-  };
-
-  bool ok_next;
-  fetch(pg_begin, ok_next);
-  for (int pg = pg_begin; pg < pg_end; ++pg) {
-    u32x4 kc[KK];
-    u32x2 vc[NB];
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) kc[kk] = kf[kk];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) vc[nb] = vf[nb];
-    const bool ok = ok_next;
-    if (pg + 1 < pg_end) fetch(pg + 1, ok_next);
-    if (!ok) continue;
+    for (int nb = 0; nb < NB; ++nb) vf[nb] = *(const u32x2 *)(kb + v_off + (nb * 16 + hl) * kPage + rq * 4);
+  }
+  for (; pg < pg_end; pg += 4) {
+    const int nxt = pg + 4;
+    bool ok_n = false;
+    const uint16_t *kb_n = nxt < pg_end ? page_ptr(nxt, ok_n) : nullptr;
 
     f32x4 s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) s = mfma_16x16x32(__builtin_bit_cast(bf16x8, kc[kk]), qf[kk], s);
+    for (int kk = 0; kk < KK; ++kk) s = mfma_16x16x32(__builtin_bit_cast(bf16x8, kf[kk]), qf[kk], s);
+    if (kb_n) {
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) kf[kk] = *(const u32x4 *)(kb_n + hl * D + kk * 32 + rq * 8);
+    }
 
     const int tok0 = pg * kPage + rq * 4;
-    const bool edge = (pg * kPage < lo) || (pg * kPage + kPage - 1 > p);
+    const bool edge = !ok || (pg * kPage < lo) || (pg * kPage + kPage - 1 > p);
     float sv[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int t = tok0 + i;
-      sv[i] = (!edge || (t >= lo && t <= p)) ? s[i] * scale_log2 : -INFINITY;
+      sv[i] = (!edge || (ok && t >= lo && t <= p)) ? s[i] * scale_log2 : -INFINITY;
     }
     float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
     mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
     mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
     const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);  // m_run = -inf -> 0
-    float pv[4];
+    if (m_new != -INFINITY) {  // false only while every page so far was an invalid id
+      const float alpha = exp2f(m_run - m_new);  // m_run = -inf -> 0
+      float pv[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) pv[i] = exp2f(sv[i] - m_new);
-    l_run = l_run * alpha + ((pv[0] + pv[1]) + (pv[2] + pv[3]));
-    m_run = m_new;
-    bf16x4 pb;
+      for (int i = 0; i < 4; ++i) pv[i] = exp2f(sv[i] - m_new);
+      l_run = l_run * alpha + ((pv[0] + pv[1]) + (pv[2] + pv[3]));
+      m_run = m_new;
+      bf16x4 pb;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) pb[i] = (__bf16)pv[i];
-    if (edge) {
-      // Zero the values of masked slots: their P is 0, but stale slots may hold
-      // non-finite bits and 0 * NaN would poison the accumulator.
-      uint32_t m01 = (tok0 >= lo && tok0 <= p ? 0xffffu : 0u) |
-                     (tok0 + 1 >= lo && tok0 + 1 <= p ? 0xffff0000u : 0u);
-      uint32_t m23 = (tok0 + 2 >= lo && tok0 + 2 <= p ? 0xffffu : 0u) |
-                     (tok0 + 3 >= lo && tok0 + 3 <= p ? 0xffff0000u : 0u);
+      for (int i = 0; i < 4; ++i) pb[i] = (__bf16)pv[i];
+      if (edge) {
+        // Zero the values of masked slots: their P is 0, but stale slots may
+        // hold non-finite bits and 0 * NaN would poison the accumulator.
+        const bool v0 = ok && tok0 >= lo && tok0 <= p, v1 = ok && tok0 + 1 >= lo && tok0 + 1 <= p;
+        const bool v2 = ok && tok0 + 2 >= lo && tok0 + 2 <= p, v3 = ok && tok0 + 3 >= lo && tok0 + 3 <= p;
+        const uint32_t m01 = (v0 ? 0xffffu : 0u) | (v1 ? 0xffff0000u : 0u);
+        const uint32_t m23 = (v2 ? 0xffffu : 0u) | (v3 ? 0xffff0000u : 0u);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          vf[nb][0] &= m01;
+          vf[nb][1] &= m23;
+        }
+      }
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        vc[nb][0] &= m01;
-        vc[nb][1] &= m23;
+        acc[nb] *= alpha;
+        acc[nb] = mfma_16x16x16(__builtin_bit_cast(bf16x4, vf[nb]), pb, acc[nb]);
       }
     }
+    if (kb_n) {
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      acc[nb] *= alpha;
-      acc[nb] = mfma_16x16x16(__builtin_bit_cast(bf16x4, vc[nb]), pb, acc[nb]);
+      for (int nb = 0; nb < NB; ++nb) vf[nb] = *(const u32x2 *)(kb_n + v_off + (nb * 16 + hl) * kPage + rq * 4);
     }
+    ok = ok_n;
   }
 
   l_run += __shfl_xor(l_run, 16, kWave);
   l_run += __shfl_xor(l_run, 32, kWave);
-  if (head_ok) {
-    const int h = g * group + hl;
-    const int64_t rec = ((int64_t)b * n_q + h) * n_splits + split;
+
+  // merge the four waves of the chunk
+  if (wave > 0) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s_acc[wave - 1][nb * 4 + e][lane] = acc[nb][e];
+  }
+  if (rq == 0) {
+    s_m[wave][hl] = m_run;
+    s_l[wave][hl] = l_run;
+  }
+  __syncthreads();
+  if (wave != 0 || !head_ok) return;
+  float M = s_m[0][hl];
+#pragma unroll
+  for (int w = 1; w < 4; ++w) M = fmaxf(M, s_m[w][hl]);
+  float sc[4], L = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    sc[w] = (s_m[w][hl] == -INFINITY) ? 0.f : exp2f(s_m[w][hl] - M);
+    L += sc[w] * s_l[w][hl];
+  }
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float v = acc[nb][e] * sc[0];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) v += sc[w] * s_acc[w - 1][nb * 4 + e][lane];
+      acc[nb][e] = v;
+    }
+  const int h = g * group + hl;
+  if (chunks_b == 1) {
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    uint16_t *dst = o + ((int64_t)b * n_q + h) * D;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      u32x2 w2;
+      w2[0] = pack2(acc[nb][0] * inv, acc[nb][1] * inv);
+      w2[1] = pack2(acc[nb][2] * inv, acc[nb][3] * inv);
+      *(u32x2 *)(dst + nb * 16 + rq * 4) = w2;
+    }
+  } else {
+    const int64_t rec = ((int64_t)b * n_q + h) * n_chunks + chunk;
     float *dst = ws_acc + rec * D;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) *(f32x4 *)(dst + nb * 16 + rq * 4) = acc[nb];
     if (rq == 0) {
-      ws_ml[rec * 2] = m_run;
-      ws_ml[rec * 2 + 1] = l_run;
+      ws_ml[rec * 2] = M;
+      ws_ml[rec * 2 + 1] = L;
     }
   }
 }
 
-// o[b, h, d] = sum_s 2^(m_s - M) acc_s[d] / sum_s 2^(m_s - M) l_s over the splits
-// that hold work for sequence b.
+// One wave per (sequence, query head) with more than one chunk:
+// o[d] = sum_c 2^(m_c - M) acc_c[d] / sum_c 2^(m_c - M) l_c.
 template <int D>
 __global__ __launch_bounds__(256) void attn_merge_kernel(const float *__restrict__ ws_acc,
-                                                         const float *__restrict__ ws_ml, int n_q,
-                                                         int window, const int32_t *__restrict__ ctx_lens,
-                                                         int max_pages, int split_pages, int n_splits,
-                                                         uint16_t *__restrict__ o, int B) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)B * n_q * D) return;
-  const int d = (int)(idx % D);
-  const int h = (int)((idx / D) % n_q);
-  const int b = (int)(idx / ((int64_t)D * n_q));
+                                                         const float *__restrict__ ws_ml, int n_q, int window,
+                                                         const int32_t *__restrict__ ctx_lens, int max_pages,
+                                                         int chunk_pages, int n_chunks, uint16_t *__restrict__ o,
+                                                         int B) {
+  constexpr int DPL = D / 64;  // d values per lane
+  const int lane = threadIdx.x & 63;
+  const int64_t wid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (wid >= (int64_t)B * n_q) return;
+  const int b = (int)(wid / n_q);
   const int ctx = min(ctx_lens[b], max_pages * kPage);
+  uint16_t *dst = o + wid * D + lane * DPL;
   if (ctx < 1) {
-    o[idx] = 0;
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) dst[i] = 0;
     return;
   }
   const int p = ctx - 1;
   const int lo = window > 0 ? max(0, p - window + 1) : 0;
-  const int pages = p / kPage - lo / kPage + 1;
-  const int ns = min(n_splits, (pages + split_pages - 1) / split_pages);
-  const int64_t rec0 = ((int64_t)b * n_q + h) * n_splits;
-  float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, ws_ml[(rec0 + s) * 2]);
-  float L = 0.f, acc = 0.f;
-  if (M != -INFINITY) {
-    for (int s = 0; s < ns; ++s) {
-      const float ms = ws_ml[(rec0 + s) * 2];
-      if (ms == -INFINITY) continue;
-      const float w = exp2f(ms - M);
-      L += w * ws_ml[(rec0 + s) * 2 + 1];
-      acc += w * ws_acc[(rec0 + s) * D + d];
+  const int chunks_b = (p / kPage - lo / kPage + chunk_pages) / chunk_pages;
+  if (chunks_b <= 1) return;  // written by the chunk kernel
+  const int64_t rec0 = wid * n_chunks;
+  float mloc = -INFINITY;
+  for (int c = lane; c < chunks_b; c += 64) mloc = fmaxf(mloc, ws_ml[(rec0 + c) * 2]);
+  const float M = wave_max(mloc);
+  auto weight = [&](int c) {
+    const float mc = ws_ml[(rec0 + c) * 2];
+    return mc == -INFINITY ? 0.f : exp2f(mc - M);
+  };
+  float lsum = 0.f;
+  for (int c = lane; c < chunks_b; c += 64) lsum += weight(c) * ws_ml[(rec0 + c) * 2 + 1];
+  const float L = wave_sum(lsum);
+  float acc[DPL];
+#pragma unroll
+  for (int i = 0; i < DPL; ++i) acc[i] = 0.f;
+  const float *src = ws_acc + rec0 * D + lane * DPL;
+  for (int c0 = 0; c0 < chunks_b; c0 += 64) {
+    const float wl = (c0 + lane < chunks_b) ? weight(c0 + lane) : 0.f;
+    const int n = min(64, chunks_b - c0);
+#pragma unroll 4
+    for (int j = 0; j < n; ++j) {
+      const float w = __shfl(wl, j, kWave);
+#pragma unroll
+      for (int i = 0; i < DPL; ++i) acc[i] += w * src[(int64_t)(c0 + j) * D + i];
     }
   }
-  o[idx] = f2bf(L > 0.f ? acc / L : 0.f);
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+#pragma unroll
+  for (int i = 0; i < DPL; ++i) dst[i] = f2bf(acc[i] * inv);
 }
 
 }  // namespace
@@ -212,16 +283,17 @@ AttnPlan attn_plan(int B, int n_kv, int D, int max_pages, int window, int split_
   int span = max_pages;
   if (window > 0) span = std::min(max_pages, (window + kPage - 1) / kPage + 1);
   span = std::max(span, 1);
-  int sp = split_pages_req;
-  if (sp <= 0) {
-    sp = 64;
-    // Enough work items to give every compute unit many waves to switch between.
-    while (sp > 4 && (int64_t)B * n_kv * ((span + sp - 1) / sp) < 8192) sp /= 2;
+  int cp = split_pages_req;
+  if (cp <= 0) {
+    // Chunks of 4..64 pages; shrink them until the batch offers enough
+    // workgroups to keep every compute unit streaming (about 8 per CU).
+    cp = 64;
+    while (cp > 4 && (int64_t)B * n_kv * ((span + cp - 1) / cp) < 8192) cp /= 2;
   }
-  sp = std::min(sp, 64);  // one page id per lane of the work item's wave
+  cp = std::min(cp, 64);  // one page id per lane of a wave
   AttnPlan plan;
-  plan.split_pages = sp;
-  plan.n_splits = (span + sp - 1) / sp;
+  plan.split_pages = cp;
+  plan.n_splits = (span + cp - 1) / cp;
   return plan;
 }
 
@@ -236,29 +308,20 @@ hipError_t launch_attention(const uint16_t *qkv, int B, int n_q, int n_kv, int D
   if (B <= 0) return hipSuccess;
   float *ws_acc = ws;
   float *ws_ml = ws + (size_t)B * n_q * plan.n_splits * D;
-  const int64_t waves = (int64_t)B * n_kv * plan.n_splits;
-  const dim3 grid((unsigned)((waves + 3) / 4));
+  const dim3 grid((unsigned)((int64_t)B * n_kv * plan.n_splits));
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
-  const int64_t outs = (int64_t)B * n_q * D;
-  const dim3 mgrid((unsigned)((outs + 255) / 256));
-  if (D == 128) {
-    hipLaunchKernelGGL(attn_split_kernel<128>, grid, dim3(256), 0, s, qkv, n_q, n_kv, window, ctx_lens,
-                       page_table, max_pages, pool, pool_pages, plan.split_pages, plan.n_splits, scale_log2,
-                       ws_acc, ws_ml, B);
+  const dim3 mgrid((unsigned)(((int64_t)B * n_q + 3) / 4));
+  auto go = [&](auto kchunk, auto kmerge) {
+    hipLaunchKernelGGL(kchunk, grid, dim3(256), 0, s, qkv, n_q, n_kv, window, ctx_lens, page_table, max_pages,
+                       pool, pool_pages, plan.split_pages, plan.n_splits, scale_log2, ws_acc, ws_ml, o, B);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_merge_kernel<128>, mgrid, dim3(256), 0, s, ws_acc, ws_ml, n_q, window, ctx_lens,
-                       max_pages, plan.split_pages, plan.n_splits, o, B);
-  } else {
-    hipLaunchKernelGGL(attn_split_kernel<64>, grid, dim3(256), 0, s, qkv, n_q, n_kv, window, ctx_lens,
-                       page_table, max_pages, pool, pool_pages, plan.split_pages, plan.n_splits, scale_log2,
-                       ws_acc, ws_ml, B);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_merge_kernel<64>, mgrid, dim3(256), 0, s, ws_acc, ws_ml, n_q, window, ctx_lens,
-                       max_pages, plan.split_pages, plan.n_splits, o, B);
-  }
-  return hipGetLastError();
+    if (e != hipSuccess || plan.n_splits <= 1) return e;
+    hipLaunchKernelGGL(kmerge, mgrid, dim3(256), 0, s, ws_acc, ws_ml, n_q, window, ctx_lens, max_pages,
+                       plan.split_pages, plan.n_splits, o, B);
+    return hipGetLastError();
+  };
+  if (D == 128) return go(attn_chunk_kernel<128>, attn_merge_kernel<128>);
+  return go(attn_chunk_kernel<64>, attn_merge_kernel<64>);
 }
 
 }  // namespace ods

@@ -40,7 +40,9 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t *x, const u
 
 // One block per sequence. RoPE (rotate-half) of the n_q + n_kv heads of
 // qkv[b] at position ctx[b] - 1, in place, and/or store of k, v into the page
-// slot of that position. cos/sin are computed once per pair index in double.
+// slot of that position. The angle p * theta^(-2i/d) is formed in double and
+// reduced modulo 2 pi there, so the fp32 sin / cos see |r| <= pi (positions
+// reach 10^5 radians, where an fp32 angle would keep only ~2 decimals).
 __global__ __launch_bounds__(256) void rope_append_kernel(uint16_t *qkv, int n_q, int n_kv, int D,
                                                           float theta, const int32_t *ctx_lens,
                                                           const int32_t *page_table, int max_pages,
@@ -51,37 +53,65 @@ __global__ __launch_bounds__(256) void rope_append_kernel(uint16_t *qkv, int n_q
   const int ctx = ctx_lens[b];
   if (ctx < 1) return;
   const int p = min(ctx, max_pages * kPage) - 1;
-  const int half = D / 2;
+  const int half = D / 2, nvh = half / 8;
   uint16_t *row = qkv + (int64_t)b * (n_q + 2 * n_kv) * D;
+
+  uint16_t *kbase = nullptr, *vbase = nullptr;
+  const int64_t blk = (int64_t)kPage * D;
+  const int slot = p % kPage;
+  if (do_append) {
+    const int page = page_table[(int64_t)b * max_pages + p / kPage];
+    if (page >= 0 && page < pool_pages) {
+      kbase = pool + (int64_t)page * 2 * n_kv * blk;
+      vbase = kbase + n_kv * blk;
+    }
+  }
   if (do_rope) {
     if (threadIdx.x < half) {
-      const double inv = pow((double)theta, -2.0 * (double)threadIdx.x / (double)D);
+      const double two_pi_hi = 6.283185307179586, two_pi_lo = 2.4492935982947064e-16;
+      const double inv = exp2(-(2.0 * threadIdx.x / D) * log2((double)theta));
       const double a = (double)p * inv;
-      cs[threadIdx.x] = (float)cos(a);
-      sn[threadIdx.x] = (float)sin(a);
-    }
-    __syncthreads();
-    const int pairs = (n_q + n_kv) * half;
-    for (int t = threadIdx.x; t < pairs; t += 256) {
-      const int h = t / half, i = t % half;
-      uint16_t *u = row + h * D;
-      const float x0 = bf2f(u[i]), x1 = bf2f(u[i + half]);
-      u[i] = f2bf(x0 * cs[i] - x1 * sn[i]);
-      u[i + half] = f2bf(x1 * cs[i] + x0 * sn[i]);
+      const double k = rint(a * (1.0 / two_pi_hi));
+      const double r = fma(-k, two_pi_lo, fma(-k, two_pi_hi, a));
+      float sv, cv;
+      sincosf((float)r, &sv, &cv);
+      cs[threadIdx.x] = cv;
+      sn[threadIdx.x] = sv;
     }
     __syncthreads();
   }
-  if (do_append) {
-    const int page = page_table[(int64_t)b * max_pages + p / kPage];
-    if (page < 0 || page >= pool_pages) return;
-    const int slot = p % kPage;
-    const int64_t blk = (int64_t)kPage * D;
-    uint16_t *kbase = pool + (int64_t)page * 2 * n_kv * blk;
-    uint16_t *vbase = kbase + n_kv * blk;
-    const uint16_t *k = row + n_q * D, *v = row + (n_q + n_kv) * D;
+  // q and k heads: rotate (if asked) 8 pairs per item; k heads also go to the cache
+  const int first = do_rope ? 0 : n_q;
+  const int items = (n_q + n_kv - first) * nvh;
+  for (int t = threadIdx.x; t < items; t += 256) {
+    const int h = first + t / nvh, i0 = (t % nvh) * 8;
+    uint16_t *u = row + h * D;
+    u32x4 x0 = *(const u32x4 *)(u + i0), x1 = *(const u32x4 *)(u + half + i0);
+    if (do_rope) {
+      u32x4 y0, y1;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = i0 + 2 * j;
+        const float a0 = bf_lo(x0[j]), a1 = bf_hi(x0[j]), b0 = bf_lo(x1[j]), b1 = bf_hi(x1[j]);
+        y0[j] = pack2(a0 * cs[i] - b0 * sn[i], a1 * cs[i + 1] - b1 * sn[i + 1]);
+        y1[j] = pack2(b0 * cs[i] + a0 * sn[i], b1 * cs[i + 1] + a1 * sn[i + 1]);
+      }
+      x0 = y0;
+      x1 = y1;
+      *(u32x4 *)(u + i0) = x0;
+      *(u32x4 *)(u + half + i0) = x1;
+    }
+    if (kbase && h >= n_q) {
+      uint16_t *dst = kbase + (h - n_q) * blk + slot * D;
+      *(u32x4 *)(dst + i0) = x0;
+      *(u32x4 *)(dst + half + i0) = x1;
+    }
+  }
+  // v heads: dim-major in the page, one element per store
+  if (vbase) {
+    const uint16_t *v = row + (n_q + n_kv) * D;
     for (int t = threadIdx.x; t < n_kv * D; t += 256) {
       const int g = t / D, i = t % D;
-      kbase[g * blk + slot * D + i] = k[t];
       vbase[g * blk + i * kPage + slot] = v[t];
     }
   }

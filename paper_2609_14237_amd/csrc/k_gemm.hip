@@ -2,9 +2,11 @@
 // expert GEMMs: C[m, n] = sum_k A[m, k] * B[n, k] (both operands K-contiguous,
 // "out x in" weights), fp32 accumulation, fused epilogues.
 //
-// Tiling: 256 threads = 4 waves; block tile BM x BN outputs, K step 64; LDS
+// Tiling: 256 threads = 4 waves; block tile BM x BN outputs, K step BK; LDS
 // double buffering (global loads of step k+1 are in flight while step k runs
-// on the matrix cores). MFMA 16x16x32 bf16: lane l holds A[m = l%16][8 k's
+// on the matrix cores). Decode GEMMs are weight-streaming (M <= 256 rows against
+// megabytes of weights), so the tile covers all rows it can and narrow outputs
+// are split along K to keep every compute unit streaming. MFMA 16x16x32 bf16: lane l holds A[m = l%16][8 k's
 // starting at (l/16)*8] and B[same k's][n = l%16]; the 16x16 fp32 result puts
 // rows (l/16)*4 .. +3 of column l%16 in lane l.
 #include "common.hpp"
@@ -14,23 +16,23 @@ namespace ods {
 
 namespace {
 
-constexpr int BK = 64;
-constexpr int LDS_STRIDE = BK + 8;  // elements; 16-byte row pad against bank conflicts
-
-template <int BM, int BN, int WM, int WN, int EPI, bool PARTIAL>
+template <int BM, int BN, int BK, int WM, int WN, int EPI, bool PARTIAL>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs p) {
+  constexpr int LDS_STRIDE = BK + 8;  // elements; 16-byte row pad against bank conflicts
   constexpr bool SILU = EPI == EPI_SILU;
   constexpr int BNL = SILU ? 2 * BN : BN;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 16, TN = WTN / 16;
   constexpr int NB = SILU ? 2 * TN : TN;  // B fragments (gate then up) per wave
-  constexpr int A_CHUNKS = BM * (BK / 8) / 256;
-  constexpr int B_CHUNKS = BNL * (BK / 8) / 256;
+  constexpr int CPR = BK / 8;  // 16-byte chunks per tile row
+  constexpr int A_CHUNKS = BM * CPR / 256;
+  constexpr int B_CHUNKS = BNL * CPR / 256;
   static_assert(WM * WN == 4, "4 waves");
-  static_assert(A_CHUNKS * 256 == BM * (BK / 8) && B_CHUNKS * 256 == BNL * (BK / 8), "tile");
+  static_assert(A_CHUNKS * 256 == BM * CPR && B_CHUNKS * 256 == BNL * CPR, "tile");
 
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDS_STRIDE];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BNL * LDS_STRIDE];
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  uint16_t(*As)[BM * LDS_STRIDE] = (uint16_t(*)[BM * LDS_STRIDE])smem;
+  uint16_t(*Bs)[BNL * LDS_STRIDE] = (uint16_t(*)[BNL * LDS_STRIDE])(smem + 2 * BM * LDS_STRIDE);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -58,7 +60,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs p) {
   int64_t b_row_off[B_CHUNKS];
 #pragma unroll
   for (int i = 0; i < B_CHUNKS; ++i) {
-    const int r = (tid + i * 256) >> 3;
+    const int r = (tid + i * 256) / CPR;
     int n, row;
     if (SILU) {
       n = n0 + (r % BN);
@@ -81,28 +83,29 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs p) {
     auto load = [&](int k0) {
 #pragma unroll
       for (int i = 0; i < A_CHUNKS; ++i) {
-        const int c = tid + i * 256, r = c >> 3, kc = (c & 7) * 8;
+        const int c = tid + i * 256, r = c / CPR, kc = (c % CPR) * 8;
         const int m = m0 + r, k = k0 + kc;
         ra[i] = (m < m_end && k < k_end) ? *(const u32x4 *)(p.A + (int64_t)m * p.lda + k)
                                          : u32x4{0u, 0u, 0u, 0u};
       }
 #pragma unroll
       for (int i = 0; i < B_CHUNKS; ++i) {
-        const int c = tid + i * 256, kc = (c & 7) * 8;
+        const int c = tid + i * 256, kc = (c % CPR) * 8;
         const int k = k0 + kc;
-        rb[i] = (b_row_off[i] >= 0 && k < k_end) ? *(const u32x4 *)(Bg + b_row_off[i] + k)
-                                                 : u32x4{0u, 0u, 0u, 0u};
+        rb[i] = (b_row_off[i] >= 0 && k < k_end)
+                    ? __builtin_nontemporal_load((const u32x4 *)(Bg + b_row_off[i] + k))
+                    : u32x4{0u, 0u, 0u, 0u};
       }
     };
     auto store = [&](int buf) {
 #pragma unroll
       for (int i = 0; i < A_CHUNKS; ++i) {
-        const int c = tid + i * 256, r = c >> 3, kc = (c & 7) * 8;
+        const int c = tid + i * 256, r = c / CPR, kc = (c % CPR) * 8;
         *(u32x4 *)&As[buf][r * LDS_STRIDE + kc] = ra[i];
       }
 #pragma unroll
       for (int i = 0; i < B_CHUNKS; ++i) {
-        const int c = tid + i * 256, r = c >> 3, kc = (c & 7) * 8;
+        const int c = tid + i * 256, r = c / CPR, kc = (c % CPR) * 8;
         *(u32x4 *)&Bs[buf][r * LDS_STRIDE + kc] = rb[i];
       }
     };
@@ -174,68 +177,94 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs p) {
   }
 }
 
-// Sum split-K partials and apply the epilogue.
+// Sum split-K partials and apply the epilogue, 4 outputs per thread (N % 4 == 0).
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs p) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t total = (int64_t)p.M * p.N;
-  if (idx >= total) return;
-  const int m = (int)(idx / p.N), n = (int)(idx % p.N);
+  if (q * 4 >= total) return;
+  const int m = (int)(q * 4 / p.N), n = (int)(q * 4 % p.N);
   const int64_t ncols = EPI == EPI_SILU ? 2 * (int64_t)p.N : p.N;
-  float v = 0.f, up = 0.f;
+  f32x4 v = {0.f, 0.f, 0.f, 0.f}, up = {0.f, 0.f, 0.f, 0.f};
   for (int s = 0; s < p.splits; ++s) {
     const float *row = p.partial + ((int64_t)s * p.M + m) * ncols;
-    v += row[n];
-    if (EPI == EPI_SILU) up += row[p.N + n];
+    v += *(const f32x4 *)(row + n);
+    if (EPI == EPI_SILU) up += *(const f32x4 *)(row + p.N + n);
   }
-  if (EPI == EPI_BF16) {
-    ((uint16_t *)p.C)[(int64_t)m * p.ldc + n] = f2bf(v);
-  } else if (EPI == EPI_F32) {
-    ((float *)p.C)[(int64_t)m * p.ldc + n] = v;
-  } else if (EPI == EPI_RESID) {
-    uint16_t *c = (uint16_t *)p.C + (int64_t)m * p.ldc + n;
-    *c = f2bf(bf2f(*c) + v);
-  } else {
-    ((uint16_t *)p.C)[(int64_t)m * p.ldc + n] = f2bf(silu(v) * up);
+  if (EPI == EPI_F32) {
+    *(f32x4 *)((float *)p.C + (int64_t)m * p.ldc + n) = v;
+    return;
   }
+  uint16_t *c = (uint16_t *)p.C + (int64_t)m * p.ldc + n;
+  if (EPI == EPI_RESID) {
+    const u32x2 old = *(const u32x2 *)c;
+    v[0] += bf_lo(old[0]);
+    v[1] += bf_hi(old[0]);
+    v[2] += bf_lo(old[1]);
+    v[3] += bf_hi(old[1]);
+  } else if (EPI == EPI_SILU) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = silu(v[e]) * up[e];
+  }
+  u32x2 o;
+  o[0] = pack2(v[0], v[1]);
+  o[1] = pack2(v[2], v[3]);
+  *(u32x2 *)c = o;
 }
 
-constexpr int kBM = 64, kBN = 64;
+constexpr int kBM = 64, kBK = 128;
+
+size_t lds_bytes(int BM, int BN, int BK, bool silu) { return (size_t)2 * (BM + (silu ? 2 : 1) * BN) * (BK + 8) * 2; }
+
+template <int BN, int EPI, bool PARTIAL>
+hipError_t launch_tile(const GemmArgs &a, dim3 grid, hipStream_t s) {
+  auto kern = gemm_kernel<kBM, BN, kBK, 2, 2, EPI, PARTIAL>;
+  const size_t lds = lds_bytes(kBM, BN, kBK, EPI == EPI_SILU);
+  static bool attr_set = false;  // the attribute only raises a per-kernel limit; setting it twice is harmless
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, grid, dim3(256), lds, s, a);
+  return hipGetLastError();
+}
+
+// Output tile width: 32 columns for narrow outputs (more blocks), 64 otherwise.
+// SiLU-gated outputs count gate and up rows, so their tile is half as wide.
+int tile_n(int N, int epi) { return (epi == EPI_SILU ? 2 * N : N) <= 8192 ? 32 : (epi == EPI_SILU ? 32 : 64); }
 
 template <int EPI>
 hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
-  const int n_tiles = (a.N + kBN - 1) / kBN;
-  if (a.group_off) {
-    dim3 grid(n_tiles, 1, a.groups);
-    hipLaunchKernelGGL((gemm_kernel<kBM, kBN, 2, 2, EPI, false>), grid, dim3(256), 0, s, a);
-    return hipGetLastError();
-  }
-  const int m_tiles = (a.M + kBM - 1) / kBM;
-  if (a.splits > 1) {
-    dim3 grid(n_tiles, m_tiles, a.splits);
-    hipLaunchKernelGGL((gemm_kernel<kBM, kBN, 2, 2, EPI, true>), grid, dim3(256), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const int64_t total = (int64_t)a.M * a.N;
-    hipLaunchKernelGGL((splitk_reduce_kernel<EPI>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
-                       s, a);
-    return hipGetLastError();
-  }
-  dim3 grid(n_tiles, m_tiles, 1);
-  hipLaunchKernelGGL((gemm_kernel<kBM, kBN, 2, 2, EPI, false>), grid, dim3(256), 0, s, a);
+  const int bn = tile_n(a.N, EPI);
+  const int n_tiles = (a.N + bn - 1) / bn;
+  const int m_tiles = a.group_off ? 1 : (a.M + kBM - 1) / kBM;
+  const bool part = !a.group_off && a.splits > 1;
+  dim3 grid(n_tiles, m_tiles, a.group_off ? a.groups : (part ? a.splits : 1));
+  hipError_t e;
+  if (bn == 32)
+    e = part ? launch_tile<32, EPI, true>(a, grid, s) : launch_tile<32, EPI, false>(a, grid, s);
+  else
+    e = part ? launch_tile<64, EPI, true>(a, grid, s) : launch_tile<64, EPI, false>(a, grid, s);
+  if (e != hipSuccess || !part) return e;
+  const int64_t quads = (int64_t)a.M * a.N / 4;
+  hipLaunchKernelGGL((splitk_reduce_kernel<EPI>), dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
 int gemm_splits(int M, int N, int K, int epi) {
-  (void)epi;
-  const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
-  const int steps = (K + BK - 1) / BK;
+  if (N % 4 != 0) return 1;  // the reduce works on 4-column groups
+  const int bn = tile_n(N, epi);
+  const int tiles = ((M + kBM - 1) / kBM) * ((N + bn - 1) / bn);
+  const int steps = (K + kBK - 1) / kBK;
   int s = 1;
-  // Narrow outputs leave most of the 256 compute units idle: split K until
-  // there are at least ~512 blocks, keeping >= 8 K steps per block.
-  while (tiles * s * 2 <= 512 && steps / (s * 2) >= 8) s *= 2;
+  // Too few tiles leaves HBM idle: split K up to 4 ways until there are about
+  // two blocks per compute unit, keeping at least 8 K steps per block. The
+  // SiLU-gated GEMM is wide enough at decode batches and skips the extra pass.
+  const int want = epi == EPI_SILU ? 256 : 512;
+  while (tiles * s < want && s < 4 && steps / (s * 2) >= 8) s *= 2;
   return s;
 }
 

@@ -92,9 +92,10 @@ class Setup:
 
     # ---------------------------------------------------------------- oracle side
     def oracle_inputs(self, rows=None):
-        """float64 copies of every input (optionally only the given rows and their pages)."""
+        """float64 copies of every input (optionally only the given rows and their pages).
+        Per-expert weight stacks are converted lazily, one expert at a time."""
         rows = np.arange(self.w.batch) if rows is None else np.asarray(rows)
-        weights = [{k: f64(v) for k, v in w.items()} for w in self.weights]
+        weights = [{k: (LazyF64(v) if v.dim() == 3 else f64(v)) for k, v in w.items()} for w in self.weights]
         n_pages = [-(-int(self.ctx[b]) // 16) for b in rows]
         pages = np.concatenate([self.page_table[b, :n] for b, n in zip(rows, n_pages)])
         sub_table = np.full((len(rows), self.max_pages), -1, dtype=np.int32)
@@ -106,6 +107,21 @@ class Setup:
         pools = [f64(p.index_select(0, idx)) for p in self.pools]
         return dict(weights=weights, pools=pools, page_table=sub_table, ctx=self.ctx[rows].copy(),
                     x=f64(self.x[torch.from_numpy(rows).to(self.device)]))
+
+
+class LazyF64:
+    """Indexable float64 view of a device tensor stack: [e] converts one slice."""
+
+    def __init__(self, t):
+        self.t = t
+        self.shape = tuple(t.shape)
+        self._cache = {}
+
+    def __getitem__(self, e):
+        e = int(e)
+        if e not in self._cache:
+            self._cache[e] = f64(self.t[e])
+        return self._cache[e]
 
 
 def oracle_run(inp, cfgs, a, b, live=None):
