@@ -33,7 +33,15 @@ namespace ods {
 namespace {
 
 template <int D>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) void attn_chunk_kernel(
+struct PageRegs {
+  u32x4 k[D / 32];  // K rows: lane l holds K[t = l%16][kk*32 + (l/16)*8 .. +8]
+  u32x2 v[D / 16];  // V dim-major: lane l holds V[d = nb*16 + l%16][t = (l/16)*4 .. +4]
+  int pg;           // page index within the sequence (uniform)
+  bool ok;          // page id inside the pool (uniform)
+};
+
+template <int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) void attn_chunk_kernel(
     const uint16_t *__restrict__ qkv, int n_q, int n_kv, int window, const int32_t *__restrict__ ctx_lens,
     const int32_t *__restrict__ page_table, int max_pages, const uint16_t *__restrict__ pool,
     int64_t pool_pages, int chunk_pages, int n_chunks, float scale_log2, float *__restrict__ ws_acc,
@@ -44,26 +52,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
   __shared__ float s_acc[3][NB * 4][64];  // waves 1..3, [register][lane]: conflict-free
   __shared__ float s_m[4][16], s_l[4][16];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int item = blockIdx.x;
-  const int chunk = item % n_chunks;
-  const int g = (item / n_chunks) % n_kv;
-  const int b = item / (n_chunks * n_kv);
-  if (b >= B) return;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: keeps control flow scalar
   const int group = n_q / n_kv;
+  const int hl = lane & 15;  // head within the group (MFMA column)
+  const int rq = lane >> 4;  // lane row-quad
+  const bool head_ok = hl < group;
+  const int64_t n_items = (int64_t)n_chunks * B * n_kv;
+  // Persistent blocks stride over the virtual items, chunk index slowest, so
+  // every block sees a similar mix of sequences and an empty item (a chunk
+  // past the end of a short window) costs one lookup instead of a launch.
+  for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
+  const int chunk = (int)(item / ((int64_t)B * n_kv));
+  const int bg = (int)(item % ((int64_t)B * n_kv));
+  const int g = bg % n_kv;
+  const int b = bg / n_kv;
   const int ctx = min(ctx_lens[b], max_pages * kPage);
-  if (ctx < 1) return;
+  if (ctx < 1) continue;
   const int p = ctx - 1;
   const int lo = window > 0 ? max(0, p - window + 1) : 0;
   const int first_page = lo / kPage, last_page = p / kPage;
   const int pg_begin = first_page + chunk * chunk_pages;
-  if (pg_begin > last_page) return;  // uniform over the block
+  if (pg_begin > last_page) continue;  // uniform over the block
   const int pg_end = min(pg_begin + chunk_pages, last_page + 1);
   const int chunks_b = (last_page - first_page + chunk_pages) / chunk_pages;
-
-  const int hl = lane & 15;  // head within the group (MFMA column)
-  const int rq = lane >> 4;  // lane row-quad
-  const bool head_ok = hl < group;
+  // this wave's contiguous share of the chunk
+  const int per_wave = (pg_end - pg_begin + 3) / 4;
+  const int w_begin = min(pg_end, pg_begin + wave * per_wave);
+  const int n_my = min(pg_end, w_begin + per_wave) - w_begin;
 
   bf16x8 qf[KK];
   {
@@ -84,39 +100,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
   const uint16_t *pool_g = pool + (int64_t)g * BLK;
   const int64_t page_stride = 2 * (int64_t)n_kv * BLK;
   const int64_t v_off = (int64_t)n_kv * BLK;
-  // Page ids of the chunk, one per lane (chunk_pages <= 64), broadcast with
-  // readlane so the K/V loads never wait on a dependent scalar load.
-  const int my_page = (lane < pg_end - pg_begin) ? pt[pg_begin + lane] : -1;
-  auto page_ptr = [&](int pg, bool &ok) {
-    int page = __builtin_amdgcn_readlane(my_page, pg - pg_begin);
-    ok = (unsigned)page < (unsigned long long)pool_pages;
-    return pool_g + (int64_t)(ok ? page : 0) * page_stride;
+  // Page ids of this wave's pages, one per lane (at most 16), broadcast with readlane.
+  const int my_page = (lane < n_my) ? pt[w_begin + lane] : -1;
+
+  // Issue the loads of this wave's page j (clamped to its last page so the
+  // loads are unconditional and the compiler can count them in flight).
+  auto issue = [&](PageRegs<D> &R, int j) {
+    const int jj = min(j, n_my - 1);
+    int page = __builtin_amdgcn_readlane(my_page, jj);
+    R.pg = w_begin + j;
+    R.ok = (unsigned)page < (unsigned long long)pool_pages;
+    const uint16_t *kb = pool_g + (int64_t)(R.ok ? page : 0) * page_stride;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) R.k[kk] = *(const u32x4 *)(kb + hl * D + kk * 32 + rq * 8);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) R.v[nb] = *(const u32x2 *)(kb + v_off + (nb * 16 + hl) * kPage + rq * 4);
   };
-
-  u32x4 kf[KK];
-  u32x2 vf[NB];
-  int pg = pg_begin + wave;
-  bool ok = false;
-  if (pg < pg_end) {
-    const uint16_t *kb = page_ptr(pg, ok);
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) kf[kk] = *(const u32x4 *)(kb + hl * D + kk * 32 + rq * 8);
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) vf[nb] = *(const u32x2 *)(kb + v_off + (nb * 16 + hl) * kPage + rq * 4);
-  }
-  for (; pg < pg_end; pg += 4) {
-    const int nxt = pg + 4;
-    bool ok_n = false;
-    const uint16_t *kb_n = nxt < pg_end ? page_ptr(nxt, ok_n) : nullptr;
-
+  auto consume = [&](PageRegs<D> &R) {
+    const int pg = R.pg;
+    const bool ok = R.ok;
     f32x4 s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) s = mfma_16x16x32(__builtin_bit_cast(bf16x8, kf[kk]), qf[kk], s);
-    if (kb_n) {
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) kf[kk] = *(const u32x4 *)(kb_n + hl * D + kk * 32 + rq * 8);
-    }
-
+    for (int kk = 0; kk < KK; ++kk) s = mfma_16x16x32(__builtin_bit_cast(bf16x8, R.k[kk]), qf[kk], s);
     const int tok0 = pg * kPage + rq * 4;
     const bool edge = !ok || (pg * kPage < lo) || (pg * kPage + kPage - 1 > p);
     float sv[4];
@@ -129,40 +134,47 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
     mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
     mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
     const float m_new = fmaxf(m_run, mx);
-    if (m_new != -INFINITY) {  // false only while every page so far was an invalid id
-      const float alpha = exp2f(m_run - m_new);  // m_run = -inf -> 0
-      float pv[4];
+    if (m_new == -INFINITY) return;  // only while every page so far had an invalid id
+    const float alpha = exp2f(m_run - m_new);  // m_run = -inf -> 0
+    float pv[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) pv[i] = exp2f(sv[i] - m_new);
-      l_run = l_run * alpha + ((pv[0] + pv[1]) + (pv[2] + pv[3]));
-      m_run = m_new;
-      bf16x4 pb;
+    for (int i = 0; i < 4; ++i) pv[i] = exp2f(sv[i] - m_new);
+    l_run = l_run * alpha + ((pv[0] + pv[1]) + (pv[2] + pv[3]));
+    m_run = m_new;
+    bf16x4 pb;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) pb[i] = (__bf16)pv[i];
-      if (edge) {
-        // Zero the values of masked slots: their P is 0, but stale slots may
-        // hold non-finite bits and 0 * NaN would poison the accumulator.
-        const bool v0 = ok && tok0 >= lo && tok0 <= p, v1 = ok && tok0 + 1 >= lo && tok0 + 1 <= p;
-        const bool v2 = ok && tok0 + 2 >= lo && tok0 + 2 <= p, v3 = ok && tok0 + 3 >= lo && tok0 + 3 <= p;
-        const uint32_t m01 = (v0 ? 0xffffu : 0u) | (v1 ? 0xffff0000u : 0u);
-        const uint32_t m23 = (v2 ? 0xffffu : 0u) | (v3 ? 0xffff0000u : 0u);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          vf[nb][0] &= m01;
-          vf[nb][1] &= m23;
-        }
-      }
+    for (int i = 0; i < 4; ++i) pb[i] = (__bf16)pv[i];
+    if (edge) {
+      // Zero the values of masked slots: their P is 0, but stale slots may
+      // hold non-finite bits and 0 * NaN would poison the accumulator.
+      const bool v0 = ok && tok0 >= lo && tok0 <= p, v1 = ok && tok0 + 1 >= lo && tok0 + 1 <= p;
+      const bool v2 = ok && tok0 + 2 >= lo && tok0 + 2 <= p, v3 = ok && tok0 + 3 >= lo && tok0 + 3 <= p;
+      const uint32_t m01 = (v0 ? 0xffffu : 0u) | (v1 ? 0xffff0000u : 0u);
+      const uint32_t m23 = (v2 ? 0xffffu : 0u) | (v3 ? 0xffff0000u : 0u);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        acc[nb] *= alpha;
-        acc[nb] = mfma_16x16x16(__builtin_bit_cast(bf16x4, vf[nb]), pb, acc[nb]);
+        R.v[nb][0] &= m01;
+        R.v[nb][1] &= m23;
       }
     }
-    if (kb_n) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) vf[nb] = *(const u32x2 *)(kb_n + v_off + (nb * 16 + hl) * kPage + rq * 4);
+    for (int nb = 0; nb < NB; ++nb) {
+      acc[nb] *= alpha;
+      acc[nb] = mfma_16x16x16(__builtin_bit_cast(bf16x4, R.v[nb]), pb, acc[nb]);
     }
-    ok = ok_n;
+  };
+
+  if (n_my > 0) {
+    // Two pages in flight per wave: while page j is consumed, j+1 is loading.
+    PageRegs<D> R0, R1;
+    issue(R0, 0);
+    issue(R1, 1);
+    for (int j = 0; j < n_my; j += 2) {
+      consume(R0);
+      issue(R0, j + 2);
+      if (j + 1 < n_my) consume(R1);
+      issue(R1, j + 3);
+    }
   }
 
   l_run += __shfl_xor(l_run, 16, kWave);
@@ -180,7 +192,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
     s_l[wave][hl] = l_run;
   }
   __syncthreads();
-  if (wave != 0 || !head_ok) return;
+  if (wave == 0 && head_ok) {
   float M = s_m[0][hl];
 #pragma unroll
   for (int w = 1; w < 4; ++w) M = fmaxf(M, s_m[w][hl]);
@@ -219,6 +231,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
       ws_ml[rec * 2] = M;
       ws_ml[rec * 2 + 1] = L;
     }
+  }
+  }
+  __syncthreads();  // the next item reuses the merge buffers
   }
 }
 
@@ -278,6 +293,19 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float *__restrict
 
 }  // namespace
 
+// Compute units of the current device (queried once per process and device).
+int num_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
 AttnPlan attn_plan(int B, int n_kv, int D, int max_pages, int window, int split_pages_req) {
   (void)D;
   int span = max_pages;
@@ -285,12 +313,17 @@ AttnPlan attn_plan(int B, int n_kv, int D, int max_pages, int window, int split_
   span = std::max(span, 1);
   int cp = split_pages_req;
   if (cp <= 0) {
-    // Chunks of 4..64 pages; shrink them until the batch offers enough
-    // workgroups to keep every compute unit streaming (about 8 per CU).
-    cp = 64;
-    while (cp > 4 && (int64_t)B * n_kv * ((span + cp - 1) / cp) < 8192) cp /= 2;
+    // A sliding window that fits in 128 pages is one chunk (no merge pass);
+    // otherwise 128-page chunks, halved while the batch offers fewer items
+    // than the persistent grid has blocks.
+    if (window > 0 && span <= 128) {
+      cp = span;
+    } else {
+      cp = 128;
+      while (cp > 8 && (int64_t)B * n_kv * ((span + cp - 1) / cp) < 3 * num_cus()) cp /= 2;
+    }
   }
-  cp = std::min(cp, 64);  // one page id per lane of a wave
+  cp = std::min(cp, 128);  // a wave's share of a chunk must fit one page id per lane
   AttnPlan plan;
   plan.split_pages = cp;
   plan.n_splits = (span + cp - 1) / cp;
@@ -308,7 +341,10 @@ hipError_t launch_attention(const uint16_t *qkv, int B, int n_q, int n_kv, int D
   if (B <= 0) return hipSuccess;
   float *ws_acc = ws;
   float *ws_ml = ws + (size_t)B * n_q * plan.n_splits * D;
-  const dim3 grid((unsigned)((int64_t)B * n_kv * plan.n_splits));
+  // Persistent grid: three 4-wave blocks per compute unit (the occupancy the
+  // kernel's registers allow), never more blocks than items.
+  const int64_t n_items = (int64_t)B * n_kv * plan.n_splits;
+  const dim3 grid((unsigned)std::min<int64_t>(n_items, 3 * num_cus()));
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
   const dim3 mgrid((unsigned)(((int64_t)B * n_q + 3) / 4));
   auto go = [&](auto kchunk, auto kmerge) {

@@ -34,7 +34,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs p) {
   uint16_t(*As)[BM * LDS_STRIDE] = (uint16_t(*)[BM * LDS_STRIDE])smem;
   uint16_t(*Bs)[BNL * LDS_STRIDE] = (uint16_t(*)[BNL * LDS_STRIDE])(smem + 2 * BM * LDS_STRIDE);
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform
   const int wm = wave / WN, wn = wave % WN;
   const int n0 = blockIdx.x * BN;
 
@@ -216,10 +217,10 @@ constexpr int kBM = 64, kBK = 128;
 
 size_t lds_bytes(int BM, int BN, int BK, bool silu) { return (size_t)2 * (BM + (silu ? 2 : 1) * BN) * (BK + 8) * 2; }
 
-template <int BN, int EPI, bool PARTIAL>
+template <int BM, int BN, int BK, int EPI, bool PARTIAL>
 hipError_t launch_tile(const GemmArgs &a, dim3 grid, hipStream_t s) {
-  auto kern = gemm_kernel<kBM, BN, kBK, 2, 2, EPI, PARTIAL>;
-  const size_t lds = lds_bytes(kBM, BN, kBK, EPI == EPI_SILU);
+  auto kern = gemm_kernel<BM, BN, BK, 2, 2, EPI, PARTIAL>;
+  const size_t lds = lds_bytes(BM, BN, BK, EPI == EPI_SILU);
   static bool attr_set = false;  // the attribute only raises a per-kernel limit; setting it twice is harmless
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -238,14 +239,21 @@ template <int EPI>
 hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
   const int bn = tile_n(a.N, EPI);
   const int n_tiles = (a.N + bn - 1) / bn;
-  const int m_tiles = a.group_off ? 1 : (a.M + kBM - 1) / kBM;
-  const bool part = !a.group_off && a.splits > 1;
-  dim3 grid(n_tiles, m_tiles, a.group_off ? a.groups : (part ? a.splits : 1));
+  if (a.group_off) {
+    // Expert row groups average B*k/E rows (64 at the MoE workload): a
+    // 128-row tile covers a whole group, so each expert's weights stream once.
+    dim3 grid(n_tiles, 1, a.groups);
+    return bn == 32 ? launch_tile<128, 32, 64, EPI, false>(a, grid, s)
+                    : launch_tile<128, 64, 64, EPI, false>(a, grid, s);
+  }
+  const int m_tiles = (a.M + kBM - 1) / kBM;
+  const bool part = a.splits > 1;
+  dim3 grid(n_tiles, m_tiles, part ? a.splits : 1);
   hipError_t e;
   if (bn == 32)
-    e = part ? launch_tile<32, EPI, true>(a, grid, s) : launch_tile<32, EPI, false>(a, grid, s);
+    e = part ? launch_tile<kBM, 32, kBK, EPI, true>(a, grid, s) : launch_tile<kBM, 32, kBK, EPI, false>(a, grid, s);
   else
-    e = part ? launch_tile<64, EPI, true>(a, grid, s) : launch_tile<64, EPI, false>(a, grid, s);
+    e = part ? launch_tile<kBM, 64, kBK, EPI, true>(a, grid, s) : launch_tile<kBM, 64, kBK, EPI, false>(a, grid, s);
   if (e != hipSuccess || !part) return e;
   const int64_t quads = (int64_t)a.M * a.N / 4;
   hipLaunchKernelGGL((splitk_reduce_kernel<EPI>), dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, s, a);
