@@ -178,6 +178,175 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs p) {
   }
 }
 
+// Large-M variant (M > 64: the 256-row decode batch, the 512-row MoE
+// attention projections): 512 threads = 8 waves as 4 (M) x 2 (N), block tile
+// BM x BN with BN = 128 columns of B rows (SiLU: 64 gate + 64 up rows), wave
+// tile (BM/4) x 64. The whole batch fits one or two M tiles, so the weights
+// stream from HBM once. Pipeline: step k+1 arrives in registers while step k
+// is on the matrix cores; its LDS stores are issued between the two MFMA
+// halves of step k (into the buffer the previous barrier freed) so the LDS,
+// matrix and load units overlap; one barrier per K step.
+template <int BM, int EPI, bool PARTIAL>
+__global__ __launch_bounds__(512) void gemm_big_kernel(GemmArgs p) {
+  constexpr int BK = 64, LS = BK + 8, CPR = BK / 8;
+  constexpr bool SILU = EPI == EPI_SILU;
+  constexpr int BNL = 128;                 // B-tile rows
+  constexpr int BN = SILU ? 64 : 128;      // output columns per block
+  constexpr int WTM = BM / 4, TM = WTM / 16;
+  constexpr int TN = SILU ? 2 : 4;         // output n-tiles per wave
+  constexpr int NB = SILU ? 4 : 4;         // B fragments per wave (gate+up for SiLU)
+  constexpr int AC = BM * CPR / 512, BC = BNL * CPR / 512;
+  static_assert(AC * 512 == BM * CPR && BC * 512 == BNL * CPR, "tile");
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  uint16_t *As = smem;
+  uint16_t *Bs = smem + 2 * BM * LS;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
+  int k_begin = 0, k_end = p.K, split = 0;
+  if (PARTIAL) {
+    split = blockIdx.z;
+    const int steps = (p.K + BK - 1) / BK;
+    const int per = (steps + p.splits - 1) / p.splits;
+    k_begin = split * per * BK;
+    k_end = min(p.K, k_begin + per * BK);
+  }
+  const int nk = max(0, (k_end - k_begin + BK - 1) / BK);
+
+  // Sources of this thread's chunks; rows outside M / N read a valid row and are zeroed at the LDS store.
+  const uint16_t *asrc[AC], *bsrc[BC];
+  bool aok[AC], bok[BC];
+#pragma unroll
+  for (int i = 0; i < AC; ++i) {
+    const int c = tid + i * 512, m = m0 + c / CPR;
+    aok[i] = m < p.M;
+    asrc[i] = p.A + (int64_t)(aok[i] ? m : 0) * p.lda + (c % CPR) * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < BC; ++i) {
+    const int c = tid + i * 512, r = c / CPR;
+    int n, row;
+    if (SILU) {
+      n = n0 + (r % BN);
+      row = (r < BN) ? n : p.n_up + n;
+    } else {
+      n = n0 + r;
+      row = n;
+    }
+    bok[i] = n < p.N;
+    bsrc[i] = p.B + (int64_t)(bok[i] ? row : 0) * p.ldb + (c % CPR) * 8;
+  }
+  struct St {
+    u32x4 a[AC];
+    u32x4 b[BC];
+  };
+  auto issue = [&](St &S, int kt) {
+    const int k0 = k_begin + min(kt, max(nk - 1, 0)) * BK;
+#pragma unroll
+    for (int i = 0; i < AC; ++i) {
+      const int kc = ((tid + i * 512) % CPR) * 8;
+      S.a[i] = *(const u32x4 *)(asrc[i] + (min(k0 + kc, p.K - 8) - kc));
+    }
+#pragma unroll
+    for (int i = 0; i < BC; ++i) {
+      const int kc = ((tid + i * 512) % CPR) * 8;
+      S.b[i] = __builtin_nontemporal_load((const u32x4 *)(bsrc[i] + (min(k0 + kc, p.K - 8) - kc)));
+    }
+  };
+  auto store = [&](const St &S, int kt, int buf) {
+    const int k0 = k_begin + kt * BK;
+#pragma unroll
+    for (int i = 0; i < AC; ++i) {
+      const int c = tid + i * 512, kc = (c % CPR) * 8;
+      *(u32x4 *)&As[buf * BM * LS + (c / CPR) * LS + kc] =
+          (aok[i] && k0 + kc < k_end) ? S.a[i] : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int i = 0; i < BC; ++i) {
+      const int c = tid + i * 512, kc = (c % CPR) * 8;
+      *(u32x4 *)&Bs[buf * BNL * LS + (c / CPR) * LS + kc] =
+          (bok[i] && k0 + kc < k_end) ? S.b[i] : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  f32x4 acc[TM][NB];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // B-tile row of wave fragment j: SiLU pairs gate tile j with up tile j (rows + BN).
+  auto brow = [&](int j) {
+    if (SILU) return (j >= TN ? BN : 0) + wn * (BN / 2) + (j % TN) * 16;
+    return wn * 64 + j * 16;
+  };
+  auto compute_ks = [&](int buf, int ks) {
+    bf16x8 af[TM], bfr[NB];
+    const int col = ks * 32 + (lane >> 4) * 8;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+      af[i] = __builtin_bit_cast(bf16x8, *(const u32x4 *)&As[buf * BM * LS + (wm * WTM + i * 16 + (lane & 15)) * LS + col]);
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      bfr[j] = __builtin_bit_cast(bf16x8, *(const u32x4 *)&Bs[buf * BNL * LS + (brow(j) + (lane & 15)) * LS + col]);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j) acc[i][j] = mfma_16x16x32(af[i], bfr[j], acc[i][j]);
+  };
+  auto step = [&](int buf, St &Rnext, int kt) {
+    // buf holds step kt; Rnext holds step kt+1 (arriving); the other slot holds step kt+2
+    compute_ks(buf, 0);
+    store(Rnext, kt + 1, buf ^ 1);
+    compute_ks(buf, 1);
+    __syncthreads();
+    issue(Rnext, kt + 3);
+  };
+  if (nk > 0) {
+    St R0, R1;
+    issue(R0, 0);
+    issue(R1, 1);
+    store(R0, 0, 0);
+    __syncthreads();
+    issue(R0, 2);
+    for (int kt = 0; kt < nk; kt += 2) {
+      step(0, R1, kt);
+      if (kt + 1 < nk) step(1, R0, kt + 1);
+    }
+  }
+
+  // Epilogue: lane holds rows (lane>>4)*4 + e of column lane&15 of each 16x16 tile.
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + (SILU ? wn * (BN / 2) + j * 16 : wn * 64 + j * 16) + (lane & 15);
+      if (n >= p.N) continue;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int m = m0 + wm * WTM + i * 16 + (lane >> 4) * 4 + e;
+        if (m >= p.M) continue;
+        const float v = acc[i][j][e];
+        if (PARTIAL) {
+          const int64_t ncols = SILU ? 2 * (int64_t)p.N : p.N;
+          float *dst = p.partial + ((int64_t)split * p.M + m) * ncols;
+          dst[n] = v;
+          if (SILU) dst[p.N + n] = acc[i][TN + j][e];
+        } else if (EPI == EPI_BF16) {
+          ((uint16_t *)p.C)[(int64_t)m * p.ldc + n] = f2bf(v);
+        } else if (EPI == EPI_F32) {
+          ((float *)p.C)[(int64_t)m * p.ldc + n] = v;
+        } else if (EPI == EPI_RESID) {
+          uint16_t *c = (uint16_t *)p.C + (int64_t)m * p.ldc + n;
+          *c = f2bf(bf2f(*c) + v);
+        } else {
+          ((uint16_t *)p.C)[(int64_t)m * p.ldc + n] = f2bf(silu(v) * acc[i][TN + j][e]);
+        }
+      }
+    }
+  }
+}
+
 // Sum split-K partials and apply the epilogue, 4 outputs per thread (N % 4 == 0).
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs p) {
@@ -231,6 +400,20 @@ hipError_t launch_tile(const GemmArgs &a, dim3 grid, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int BM, int EPI, bool PARTIAL>
+hipError_t launch_big(const GemmArgs &a, dim3 grid, hipStream_t s) {
+  auto kern = gemm_big_kernel<BM, EPI, PARTIAL>;
+  const size_t lds = (size_t)2 * (BM + 128) * (64 + 8) * 2;
+  static bool attr_set = false;  // the attribute only raises a per-kernel limit; setting it twice is harmless
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, grid, dim3(512), lds, s, a);
+  return hipGetLastError();
+}
+
 // Output tile width: 32 columns for narrow outputs (more blocks), 64 otherwise.
 // SiLU-gated outputs count gate and up rows, so their tile is half as wide.
 int tile_n(int N, int epi) { return (epi == EPI_SILU ? 2 * N : N) <= 8192 ? 32 : (epi == EPI_SILU ? 32 : 64); }
@@ -246,14 +429,24 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
     return bn == 32 ? launch_tile<128, 32, 64, EPI, false>(a, grid, s)
                     : launch_tile<128, 64, 64, EPI, false>(a, grid, s);
   }
-  const int m_tiles = (a.M + kBM - 1) / kBM;
   const bool part = a.splits > 1;
-  dim3 grid(n_tiles, m_tiles, part ? a.splits : 1);
   hipError_t e;
+  if (a.M > kBM) {
+    const int bm = a.M > 128 ? 256 : 128;
+    const int bnb = EPI == EPI_SILU ? 64 : 128;
+    dim3 grid((a.N + bnb - 1) / bnb, (a.M + bm - 1) / bm, part ? a.splits : 1);
+    if (bm == 256)
+      e = part ? launch_big<256, EPI, true>(a, grid, s) : launch_big<256, EPI, false>(a, grid, s);
+    else
+      e = part ? launch_big<128, EPI, true>(a, grid, s) : launch_big<128, EPI, false>(a, grid, s);
+  } else {
+  const int m_tiles = (a.M + kBM - 1) / kBM;
+  dim3 grid(n_tiles, m_tiles, part ? a.splits : 1);
   if (bn == 32)
     e = part ? launch_tile<kBM, 32, kBK, EPI, true>(a, grid, s) : launch_tile<kBM, 32, kBK, EPI, false>(a, grid, s);
   else
     e = part ? launch_tile<kBM, 64, kBK, EPI, true>(a, grid, s) : launch_tile<kBM, 64, kBK, EPI, false>(a, grid, s);
+  }
   if (e != hipSuccess || !part) return e;
   const int64_t quads = (int64_t)a.M * a.N / 4;
   hipLaunchKernelGGL((splitk_reduce_kernel<EPI>), dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, s, a);
@@ -264,6 +457,16 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
 
 int gemm_splits(int M, int N, int K, int epi) {
   if (N % 4 != 0) return 1;  // the reduce works on 4-column groups
+  if (M > kBM) {
+    // Large-M tiles: one 512-thread block per compute unit; split K (up to 8
+    // ways, at least 8 steps of 64 per block) until ~192 blocks are in flight.
+    const int bm = M > 128 ? 256 : 128, bn = epi == EPI_SILU ? 64 : 128;
+    const int tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+    const int steps = (K + 63) / 64;
+    int s = 1;
+    while (tiles * s < 192 && s < 8 && steps / (s * 2) >= 8) s *= 2;
+    return s;
+  }
   const int bn = tile_n(N, epi);
   const int tiles = ((M + kBM - 1) / kBM) * ((N + bn - 1) / bn);
   const int steps = (K + kBK - 1) / kBK;

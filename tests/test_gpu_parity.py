@@ -367,3 +367,31 @@ def test_dense_8b_shape_small_batch():
     s.run(6, 10)
     torch.cuda.synchronize()
     _check_layer_buffers(s, ref, w.layers[0], 5)
+
+
+# ---------------------------------------------------------------- GEMM tile paths
+
+@pytest.mark.parametrize("batch", [65, 100, 128, 200, 300])
+def test_layer_across_gemm_tile_paths(batch):
+    """Batches above 64 rows take the 512-thread large-M GEMM tiles (128 rows up
+    to 128, 256 rows above); F = 688 leaves K and SiLU-N tails, H = 640 an
+    N tail of the 128-column tile."""
+    cfg = W.LayerCfg(hidden=640, n_q=10, n_kv=2, head_dim=64, ffn=688)
+    w = W.Workload("gemm_paths", (cfg,), batch=batch, ctx_lo=1, ctx_hi=70)
+    say("gemm tile paths, batch", batch)
+    s = Setup(w, seed=12)
+    inp = s.oracle_inputs()
+    ref = oracle_run(fresh(inp), w.layers, 0, 10)
+    s.reset_resid()
+    s.run(0, 10)
+    torch.cuda.synchronize()
+    _check_layer_buffers(s, ref, cfg, batch)
+    act = O.silu(ref["gu"][:, :cfg.ffn]) * ref["gu"][:, cfg.ffn:]
+    assert_close("act", f64(s.buf("act", batch, cfg.ffn)), act)
+    # unfused gate_up (bf16 epilogue) and the standalone SiLU
+    s.reset_resid()
+    s.run(0, 8)
+    s.run(8, 10)
+    torch.cuda.synchronize()
+    assert_close("gu", f64(s.buf("gu", batch, 2 * cfg.ffn)), ref["gu"])
+    assert_close("resid (split at silu)", f64(s.buf("resid", batch, cfg.hidden)), ref["resid"])
