@@ -120,8 +120,12 @@ typedef struct {
  * ctx_lens[b] - 1; valid values are 1 .. max_pages * 16 (larger values are
  * clamped, values < 1 make the row a no-op for attention and KV append).
  * page_table [batch][max_pages] int32, -1 for unused entries; page ids outside
- * [0, pool_pages) are skipped by the kernels. split_pages chooses the pages
- * per split-K work item of attn_core (0: library choice). */
+ * [0, pool_pages) are skipped by the kernels. attn_core numbers the (sequence,
+ * KV head, window page) units of the batch and gives every wave of its grid an
+ * equal contiguous range of them; split_pages fixes the range length in pages
+ * (0: library choice, the batch's pages over all waves, at least 8 each).
+ * attn_core takes batch <= 8192 and batch * n_kv * window pages < 2^30
+ * (ODS_EUNSUPPORTED otherwise). */
 typedef struct {
   int32_t batch, max_pages;
   const int32_t *ctx_lens;

@@ -39,16 +39,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs p) {
   const int wm = wave / WN, wn = wave % WN;
   const int n0 = blockIdx.x * BN;
 
-  int m_begin = 0, m_end = p.M;
+  const int m_begin = 0, m_end = p.M;
   const uint16_t *Bg = p.B;
   int k_begin = 0, k_end = p.K;
   int split = 0;
-  if (p.group_off) {
-    const int g = blockIdx.z;
-    m_begin = max(0, p.group_off[g]);        // offsets come from device memory:
-    m_end = min(p.M, p.group_off[g + 1]);    // never step outside the M rows
-    Bg += (int64_t)g * p.b_group_stride;
-  } else if (PARTIAL) {
+  if (PARTIAL) {
     split = blockIdx.z;
     const int steps = (p.K + BK - 1) / BK;
     const int per = (steps + p.splits - 1) / p.splits;
@@ -185,9 +180,13 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs p) {
 // stream from HBM once. Pipeline: step k+1 arrives in registers while step k
 // is on the matrix cores; its LDS stores are issued between the two MFMA
 // halves of step k (into the buffer the previous barrier freed) so the LDS,
-// matrix and load units overlap; one barrier per K step.
+// matrix and load units overlap; one barrier per K step. A 128-row tile's
+// LDS (74 KB) leaves room for two blocks per CU, so without split-K partials
+// (whose extra addressing would spill) its registers are capped at 128 to let
+// the second block in; a 256-row tile (110 KB) runs alone.
 template <int BM, int EPI, bool PARTIAL>
-__global__ __launch_bounds__(512) void gemm_big_kernel(GemmArgs p) {
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(BM == 128 && !PARTIAL ? 4 : 2)))
+void gemm_big_kernel(GemmArgs p) {
   constexpr int BK = 64, LS = BK + 8, CPR = BK / 8;
   constexpr bool SILU = EPI == EPI_SILU;
   constexpr int BNL = 128;                 // B-tile rows
@@ -204,7 +203,15 @@ __global__ __launch_bounds__(512) void gemm_big_kernel(GemmArgs p) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
+  const int n0 = blockIdx.x * BN;
+  int m_begin = 0, m_end = p.M;
+  const uint16_t *Bg = p.B;
+  if (p.group_off) {  // grouped (expert) GEMM: rows [off[g], off[g+1]) against weight slab g
+    const int g = blockIdx.z;
+    m_begin = max(0, p.group_off[g]);      // offsets come from device memory:
+    m_end = min(p.M, p.group_off[g + 1]);  // never step outside the M rows
+    Bg += (int64_t)g * p.b_group_stride;
+  }
   int k_begin = 0, k_end = p.K, split = 0;
   if (PARTIAL) {
     split = blockIdx.z;
@@ -216,14 +223,8 @@ __global__ __launch_bounds__(512) void gemm_big_kernel(GemmArgs p) {
   const int nk = max(0, (k_end - k_begin + BK - 1) / BK);
 
   // Sources of this thread's chunks; rows outside M / N read a valid row and are zeroed at the LDS store.
-  const uint16_t *asrc[AC], *bsrc[BC];
-  bool aok[AC], bok[BC];
-#pragma unroll
-  for (int i = 0; i < AC; ++i) {
-    const int c = tid + i * 512, m = m0 + c / CPR;
-    aok[i] = m < p.M;
-    asrc[i] = p.A + (int64_t)(aok[i] ? m : 0) * p.lda + (c % CPR) * 8;
-  }
+  const uint16_t *bsrc[BC];
+  bool bok[BC];
 #pragma unroll
   for (int i = 0; i < BC; ++i) {
     const int c = tid + i * 512, r = c / CPR;
@@ -236,7 +237,16 @@ __global__ __launch_bounds__(512) void gemm_big_kernel(GemmArgs p) {
       row = n;
     }
     bok[i] = n < p.N;
-    bsrc[i] = p.B + (int64_t)(bok[i] ? row : 0) * p.ldb + (c % CPR) * 8;
+    bsrc[i] = Bg + (int64_t)(bok[i] ? row : 0) * p.ldb + (c % CPR) * 8;
+  }
+  for (int m0 = m_begin + blockIdx.y * BM; m0 < m_end; m0 += gridDim.y * BM) {
+  const uint16_t *asrc[AC];
+  bool aok[AC];
+#pragma unroll
+  for (int i = 0; i < AC; ++i) {
+    const int c = tid + i * 512, m = m0 + c / CPR;
+    aok[i] = m < m_end;
+    asrc[i] = p.A + (int64_t)(aok[i] ? m : m_begin) * p.lda + (c % CPR) * 8;
   }
   struct St {
     u32x4 a[AC];
@@ -280,7 +290,11 @@ __global__ __launch_bounds__(512) void gemm_big_kernel(GemmArgs p) {
     if (SILU) return (j >= TN ? BN : 0) + wn * (BN / 2) + (j % TN) * 16;
     return wn * 64 + j * 16;
   };
+  // Waves whose rows all lie past the end of the tile's rows (a short expert
+  // group) skip the LDS reads and matrix work; the test is wave-uniform.
+  const bool rows_live = m0 + wm * WTM < m_end;
   auto compute_ks = [&](int buf, int ks) {
+    if (!rows_live) return;
     bf16x8 af[TM], bfr[NB];
     const int col = ks * 32 + (lane >> 4) * 8;
 #pragma unroll
@@ -325,7 +339,7 @@ __global__ __launch_bounds__(512) void gemm_big_kernel(GemmArgs p) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int m = m0 + wm * WTM + i * 16 + (lane >> 4) * 4 + e;
-        if (m >= p.M) continue;
+        if (m >= m_end) continue;
         const float v = acc[i][j][e];
         if (PARTIAL) {
           const int64_t ncols = SILU ? 2 * (int64_t)p.N : p.N;
@@ -344,6 +358,8 @@ __global__ __launch_bounds__(512) void gemm_big_kernel(GemmArgs p) {
         }
       }
     }
+  }
+  __syncthreads();  // the next M tile reuses the LDS buffers
   }
 }
 
@@ -414,6 +430,10 @@ hipError_t launch_big(const GemmArgs &a, dim3 grid, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Large-M tiles pay off when the output is wide enough to fill 128-column
+// tiles; a narrow output (the router's expert logits) stays on 64-row tiles.
+bool use_big(int M, int N) { return M > kBM && N > 128; }
+
 // Output tile width: 32 columns for narrow outputs (more blocks), 64 otherwise.
 // SiLU-gated outputs count gate and up rows, so their tile is half as wide.
 int tile_n(int N, int epi) { return (epi == EPI_SILU ? 2 * N : N) <= 8192 ? 32 : (epi == EPI_SILU ? 32 : 64); }
@@ -424,14 +444,16 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
   const int n_tiles = (a.N + bn - 1) / bn;
   if (a.group_off) {
     // Expert row groups average B*k/E rows (64 at the MoE workload): a
-    // 128-row tile covers a whole group, so each expert's weights stream once.
-    dim3 grid(n_tiles, 1, a.groups);
-    return bn == 32 ? launch_tile<128, 32, 64, EPI, false>(a, grid, s)
-                    : launch_tile<128, 64, 64, EPI, false>(a, grid, s);
+    // 128-row large-M tile covers a whole group, so each expert's weights
+    // stream once, and 128 weight rows per block keep the re-reads of the
+    // group's activations to one per 128 output columns.
+    const int bnb = EPI == EPI_SILU ? 64 : 128;
+    dim3 grid((a.N + bnb - 1) / bnb, 1, a.groups);
+    return launch_big<128, EPI, false>(a, grid, s);
   }
   const bool part = a.splits > 1;
   hipError_t e;
-  if (a.M > kBM) {
+  if (use_big(a.M, a.N)) {
     const int bm = a.M > 128 ? 256 : 128;
     const int bnb = EPI == EPI_SILU ? 64 : 128;
     dim3 grid((a.N + bnb - 1) / bnb, (a.M + bm - 1) / bm, part ? a.splits : 1);
@@ -457,7 +479,7 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
 
 int gemm_splits(int M, int N, int K, int epi) {
   if (N % 4 != 0) return 1;  // the reduce works on 4-column groups
-  if (M > kBM) {
+  if (use_big(M, N)) {
     // Large-M tiles: one 512-thread block per compute unit; split K (up to 8
     // ways, at least 8 steps of 64 per block) until ~192 blocks are in flight.
     const int bm = M > 128 ? 256 : 128, bn = epi == EPI_SILU ? 64 : 128;
@@ -474,8 +496,12 @@ int gemm_splits(int M, int N, int K, int epi) {
   // Too few tiles leaves HBM idle: split K up to 4 ways until there are about
   // two blocks per compute unit, keeping at least 8 K steps per block. The
   // SiLU-gated GEMM is wide enough at decode batches and skips the extra pass.
+  // A narrow output has few tiles at any batch: split it up to 16 ways, down
+  // to 2 K steps per block.
   const int want = epi == EPI_SILU ? 256 : 512;
-  while (tiles * s < want && s < 4 && steps / (s * 2) >= 8) s *= 2;
+  const bool narrow = N <= 128;
+  const int max_s = narrow ? 16 : 4, min_steps = narrow ? 2 : 8;
+  while (tiles * s < want && s < max_s && steps / (s * 2) >= min_steps) s *= 2;
   return s;
 }
 

@@ -65,57 +65,92 @@ __global__ __launch_bounds__(256) void topk_kernel(const float *__restrict__ log
   }
 }
 
-// Single block, T threads, stable counting sort of the n = B*k (token, slot)
-// pairs by expert: thread t owns the contiguous pair segment [t*seg, (t+1)*seg)
-// and column t of a per-(expert, thread) count table; an exclusive scan of the
-// table in expert-major order gives every pair its sorted position.
-__global__ void permute_kernel(const int32_t *__restrict__ ids, int n, int E, int32_t *__restrict__ perm,
-                               int32_t *__restrict__ slot_pos, int32_t *__restrict__ expert_off) {
-  extern __shared__ uint32_t cnt[];  // [E][T] followed by T scan slots
-  const int T = blockDim.x, t = threadIdx.x;
-  uint32_t *tot = cnt + E * T;
-  const int seg = (n + T - 1) / T;
-  const int i0 = min(n, t * seg), i1 = min(n, i0 + seg);
-  for (int e = 0; e < E; ++e) cnt[e * T + t] = 0;
+// Stable counting sort of the n = B*k (token, slot) pairs by expert in one
+// block of 16 waves. Pairs are taken in chunks of 64 (one per lane); wave w
+// owns a contiguous run of chunks. Within a chunk, the lanes holding the same
+// expert are found with one ballot per bit of the id, so a pair's rank among
+// equal ids before it is a popcount and the group's lowest lane alone updates
+// the shared counter. Pass 1 counts pairs per (expert, wave); an exclusive
+// scan of those counts in expert-major order gives each wave's first slot in
+// every expert's range; pass 2 places the pairs. Ids outside [0, E) are not
+// placed and get slot_pos -1.
+constexpr int kPermWaves = 16;
+
+__device__ __forceinline__ uint64_t same_id_lanes(int e, int bits) {
+  uint64_t m = ~0ull;
+  for (int b = 0; b < bits; ++b) {
+    const bool set = (e >> b) & 1;
+    const uint64_t v = __ballot(set);
+    m &= set ? v : ~v;
+  }
+  return m;
+}
+
+__global__ __launch_bounds__(64 * kPermWaves) void permute_kernel(const int32_t *__restrict__ ids, int n, int E,
+                                                                 int32_t *__restrict__ perm,
+                                                                 int32_t *__restrict__ slot_pos,
+                                                                 int32_t *__restrict__ expert_off) {
+  extern __shared__ uint32_t cnt[];  // [E][kPermWaves]: counts, then running slots
+  __shared__ uint32_t wave_tot[kPermWaves];
+  const int t = threadIdx.x, lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int chunks = (n + 63) / 64, per_wave = (chunks + kPermWaves - 1) / kPermWaves;
+  const int c0 = min(chunks, w * per_wave), c1 = min(chunks, c0 + per_wave);
+  int bits = 1;  // enough bits for the values 0..E (E marks an invalid id)
+  while ((1 << bits) <= E) ++bits;
+  const uint64_t below = (1ull << lane) - 1;
+  for (int j = t; j < E * kPermWaves; j += blockDim.x) cnt[j] = 0;
   __syncthreads();
-  for (int i = i0; i < i1; ++i) {
-    const int e = ids[i];
-    if ((unsigned)e < (unsigned)E) cnt[e * T + t] += 1;
+  for (int c = c0; c < c1; ++c) {
+    const int i = c * 64 + lane;
+    int e = i < n ? ids[i] : E;
+    if ((unsigned)e >= (unsigned)E) e = E;
+    const uint64_t same = same_id_lanes(e, bits);
+    if (e < E && (same & below) == 0) cnt[e * kPermWaves + w] += (uint32_t)__popcll(same);
   }
   __syncthreads();
-  // exclusive scan over the flat table; thread t scans entries [t*E, (t+1)*E)
+  // Exclusive scan over the E*16 counts; thread t scans a contiguous run.
+  const int N = E * kPermWaves, per_t = (N + (int)blockDim.x - 1) / (int)blockDim.x;
+  const int j0 = min(N, t * per_t), j1 = min(N, j0 + per_t);
   uint32_t local = 0;
-  for (int j = 0; j < E; ++j) local += cnt[t * E + j];
-  tot[t] = local;
-  __syncthreads();
-  if (t == 0) {
-    uint32_t run = 0;
-    for (int j = 0; j < T; ++j) {
-      const uint32_t x = tot[j];
-      tot[j] = run;
-      run += x;
-    }
+  for (int j = j0; j < j1; ++j) local += cnt[j];
+  uint32_t inc = local;
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(inc, d);
+    if (lane >= d) inc += y;
   }
+  if (lane == 63) wave_tot[w] = inc;
   __syncthreads();
-  uint32_t run = tot[t];
-  for (int j = 0; j < E; ++j) {
-    const uint32_t x = cnt[t * E + j];
-    cnt[t * E + j] = run;
+  uint32_t run = inc - local, total = 0;
+  for (int v = 0; v < kPermWaves; ++v) {
+    const uint32_t x = wave_tot[v];
+    if (v < w) run += x;
+    total += x;
+  }
+  for (int j = j0; j < j1; ++j) {
+    const uint32_t x = cnt[j];
+    cnt[j] = run;
     run += x;
   }
   __syncthreads();
-  for (int e = t; e < E; e += T) expert_off[e] = (int32_t)cnt[e * T];
-  if (t == T - 1) expert_off[E] = (int32_t)run;
-  __syncthreads();  // the placement below advances the counters read above
-  for (int i = i0; i < i1; ++i) {
-    const int e = ids[i];
-    if ((unsigned)e < (unsigned)E) {
-      const uint32_t pos = cnt[e * T + t]++;
-      perm[pos] = i;
-      slot_pos[i] = (int32_t)pos;
-    } else {
+  for (int e = t; e < E; e += blockDim.x) expert_off[e] = (int32_t)cnt[e * kPermWaves];
+  if (t == 0) expert_off[E] = (int32_t)total;
+  __syncthreads();  // the placement below advances the slots read above
+  for (int c = c0; c < c1; ++c) {
+    const int i = c * 64 + lane;
+    int e = i < n ? ids[i] : E;
+    if ((unsigned)e >= (unsigned)E) e = E;
+    const uint64_t same = same_id_lanes(e, bits);
+    if (i >= n) continue;
+    if (e == E) {
       slot_pos[i] = -1;
+      continue;
     }
+    const uint32_t first = cnt[e * kPermWaves + w];
+    const uint32_t pos = first + (uint32_t)__popcll(same & below);
+    perm[pos] = i;
+    slot_pos[i] = (int32_t)pos;
+    if ((same & below) == 0) cnt[e * kPermWaves + w] = first + (uint32_t)__popcll(same);
   }
 }
 
@@ -185,11 +220,9 @@ hipError_t launch_topk(const float *logits, int B, int E, int k, int32_t *ids, f
 hipError_t launch_permute(const int32_t *ids, int B, int k, int E, int32_t *perm, int32_t *slot_pos,
                           int32_t *expert_off, hipStream_t s) {
   const int n = B * k;
-  // Count table [E][T] of 32-bit counters plus T scan slots, within 64 KiB of LDS.
-  int T = 256;
-  while (T > 16 && ((size_t)E * T + T) * 4 > 65536) T /= 2;
-  const size_t lds = ((size_t)E * T + T) * sizeof(uint32_t);
-  hipLaunchKernelGGL(permute_kernel, dim3(1), dim3(T), lds, s, ids, n, E, perm, slot_pos, expert_off);
+  const size_t lds = (size_t)E * kPermWaves * sizeof(uint32_t);  // 16 KiB at E = 256
+  hipLaunchKernelGGL(permute_kernel, dim3(1), dim3(64 * kPermWaves), lds, s, ids, n, E, perm, slot_pos,
+                     expert_off);
   return hipGetLastError();
 }
 

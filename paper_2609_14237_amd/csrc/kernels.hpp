@@ -26,6 +26,9 @@ struct GemmArgs {
   float *partial;
 };
 
+// Compute units of the current device (queried once per process and device).
+int num_cus();
+
 // Split-K plan for a dense GEMM (shared by sizing and launching).
 int gemm_splits(int M, int N, int K, int epi);
 size_t gemm_partial_bytes(int M, int N, int K, int epi);
@@ -40,13 +43,17 @@ hipError_t launch_rope_append(uint16_t *qkv, int B, int n_q, int n_kv, int D, fl
                               uint16_t *pool, int64_t pool_pages, bool do_rope, bool do_append,
                               hipStream_t s);
 
-// Paged GQA decode attention (split over pages) + exact log-sum-exp merge.
+// Paged GQA decode attention (the batch's pages split evenly over the waves)
+// + exact log-sum-exp merge of sequences that span several waves.
+constexpr int kMaxAttnBatch = 8192;  // the kernel keeps a per-sequence prefix in LDS
 struct AttnPlan {
-  int split_pages;  // pages per work item
-  int n_splits;     // work items per (sequence, kv head)
+  int seg_pages;    // pages per wave range; 0: total / waves (at least 8)
+  int grid;         // workgroups of the attention kernel
+  int64_t records;  // partial-record slots per query-head group
+  bool units_ok;    // batch * n_kv * span fits the kernel's 32-bit unit index
 };
 AttnPlan attn_plan(int B, int n_kv, int D, int max_pages, int window, int split_pages_req);
-size_t attn_ws_bytes(int B, int n_q, int D, const AttnPlan &plan);
+size_t attn_ws_bytes(int B, int n_q, int n_kv, int D, const AttnPlan &plan);
 hipError_t launch_attention(const uint16_t *qkv, int B, int n_q, int n_kv, int D, int window,
                             const int32_t *ctx_lens, const int32_t *page_table, int max_pages,
                             const uint16_t *pool, int64_t pool_pages, const AttnPlan &plan,

@@ -112,7 +112,7 @@ AttnPlan plan_for(const ods_layer_cfg &c, const ods_batch *b) {
 
 size_t layer_ws_bytes(const ods_layer_cfg &c, const ods_batch *b) {
   const int B = b->batch;
-  size_t w = align_up(attn_ws_bytes(B, c.n_q, c.head_dim, plan_for(c, b)));
+  size_t w = align_up(attn_ws_bytes(B, c.n_q, c.n_kv, c.head_dim, plan_for(c, b)));
   auto g = [&](int N, int K, int epi) { w = std::max(w, align_up(gemm_partial_bytes(B, N, K, epi))); };
   g(qkv_dim(c), c.hidden, EPI_BF16);
   g(c.hidden, c.n_q * c.head_dim, EPI_RESID);
@@ -265,6 +265,11 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
         if (k == K_ATTN_CORE) {
           need.push_back({st->o, "o"});
           need.push_back({st->ws, "ws"});
+          if (B > kMaxAttnBatch)
+            return fail(ODS_EUNSUPPORTED, "layer %d: attn_core supports batch <= %d, got %d", ops[i].layer,
+                        kMaxAttnBatch, B);
+          if (!plan_for(c, batch).units_ok)
+            return fail(ODS_EUNSUPPORTED, "layer %d: batch * n_kv * window pages exceeds 2^30", ops[i].layer);
         }
         paged = true;
         break;
