@@ -75,6 +75,27 @@ def layer_accounting(cfg, ctx, B):
                 kv_bytes=kv_bytes, ffn_bytes=ffn_bytes, ffn_flops=ffn_flops)
 
 
+def handoff_bytes_per_token(cfg):
+    """Bytes per decoded token of the live set that crosses a cut after each
+    local operator of a layer (the activation interface between two stages):
+    the residual stream plus whatever later operators of the layer still read.
+    Per-batch items (expert_off) are left out."""
+    H, nq, nkv, d = cfg.hidden, cfg.n_q, cfg.n_kv, cfg.head_dim
+    resid, qkv, q, o = 2 * H, 2 * cfg.qkv_dim, 2 * nq * d, 2 * nq * d
+    if not cfg.n_experts:
+        F = cfg.ffn
+        live = [resid + 2 * H, resid + qkv, resid + qkv, resid + q, resid + o, resid,
+                resid + 2 * H, resid + 4 * F, resid + 2 * F, resid]
+    else:
+        E, k, I = cfg.n_experts, cfg.top_k, cfg.moe_ffn
+        route = 4 * k + 4 * k  # topk_w and slot_pos, read by the combine
+        live = [resid + 2 * H, resid + qkv, resid + qkv, resid + q, resid + o, resid,
+                resid + 2 * H, resid + 2 * H + 4 * E, resid + 2 * H + 8 * k,
+                resid + 2 * k * H + route, resid + 4 * k * I + route, resid + 2 * k * I + route,
+                resid + 2 * k * H + route, resid]
+    return {str(j): int(b) for j, b in enumerate(live)}
+
+
 def attn_source_hash():
     h = hashlib.sha256()
     for f in ("k_attn.hip", "common.hpp"):
@@ -291,7 +312,10 @@ def main():
                    "layers": n_layers, "copies_rotated": copies,
                    "step": "attention stage [0,6) then FFN stage [6,N) per layer"},
         "stages": {"attn": stage(t_attn, attn_bytes, attn_flops), "ffn": stage(t_ffn, ffn_bytes, ffn_flops)},
-        "roofline": {"kernel": "attn_core (split-K paged decode attention + LSE merge)",
+        "handoff": {"cut": "after local op 5 (attention stage | FFN stage)",
+                    "bytes_per_token": handoff_bytes_per_token(w.layers[0])["5"],
+                    "bytes_per_token_by_cut": handoff_bytes_per_token(w.layers[0])},
+        "roofline": {"kernel": "attn_core (paged decode attention split evenly over all waves + LSE merge)",
                      "bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK,
                      "traffic": traffic,

@@ -124,7 +124,7 @@ typedef struct {
  * KV head, window page) units of the batch and gives every wave of its grid an
  * equal contiguous range of them; split_pages fixes the range length in pages
  * (0: library choice, the batch's pages over all waves, at least 8 each).
- * attn_core takes batch <= 8192 and batch * n_kv * window pages < 2^30
+ * attn_core takes batch <= 4096 and batch * n_kv * window pages < 2^30
  * (ODS_EUNSUPPORTED otherwise). */
 typedef struct {
   int32_t batch, max_pages;

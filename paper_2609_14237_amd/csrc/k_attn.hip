@@ -42,14 +42,16 @@ template <int D>
 struct PageRegs {
   u32x4 k[D / 32];  // K rows: lane l holds K[t = l%16][kk*32 + (l/16)*8 .. +8]
   u32x2 v[D / 16];  // V dim-major: lane l holds V[d = nb*16 + l%16][t = (l/16)*4 .. +4]
+  u32x4 q[D / 32];  // the page's query heads: lane l holds q[head l%16][kk*32 + (l/16)*8 .. +8]
   int pg;           // page index within the sequence (uniform)
+  int seq;          // b * n_kv + g, -1 for a padding slot past the range (uniform)
+  int lo, p;        // attended token positions [lo, p] of the sequence (uniform)
   bool ok;          // page id inside the pool (uniform)
 };
 
-// Pages of sequence b's attended window (0 when the row is a no-op).
-__device__ __forceinline__ void window_pages(int ctx_raw, int max_pages, int window, int &p, int &lo,
-                                             int &first_page, int &n_pages) {
-  const int ctx = min(ctx_raw, max_pages * kPage);
+// Attended window of a sequence from its (clamped) context: token positions
+// [lo, p] and window pages [first_page, first_page + n_pages).
+__device__ __forceinline__ void window_of(int ctx, int window, int &p, int &lo, int &first_page, int &n_pages) {
   if (ctx < 1) {
     p = lo = first_page = n_pages = 0;
     return;
@@ -69,7 +71,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) voi
   constexpr int KK = D / 32;  // QK MFMAs per page
   constexpr int NB = D / 16;  // PV MFMAs per page
   constexpr int64_t BLK = (int64_t)kPage * D;
-  extern __shared__ int s_pre[];  // [B + 1]: first unit of sequence b (its KV head 0)
+  extern __shared__ int smem_i[];
+  int *s_pre = smem_i;          // [B + 1]: first unit of sequence b (its KV head 0)
+  int *s_ctx = smem_i + B + 1;  // [B]: context clamped to the page table
   __shared__ int s_wtot[4];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -78,15 +82,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) voi
   const int hl = lane & 15;  // head within the group (MFMA column)
   const int rq = lane >> 4;  // lane row-quad
   const bool head_ok = hl < group;
+  const int row_elems = (n_q + 2 * n_kv) * D;
 
-  // ---- unit prefix over the batch: s_pre[b] = n_kv * sum_{b' < b} pages(b')
+  // ---- per-sequence contexts and the unit prefix s_pre[b] = n_kv * sum_{b' < b} pages(b')
   {
     const int per = (B + 255) / 256;
     const int b0 = min(B, tid * per), b1 = min(B, b0 + per);
     int loc = 0;
     for (int b = b0; b < b1; ++b) {
+      const int c = min(ctx_lens[b], max_pages * kPage);
       int p, lo, fp, n;
-      window_pages(ctx_lens[b], max_pages, window, p, lo, fp, n);
+      window_of(c, window, p, lo, fp, n);
+      s_ctx[b] = c;
       loc += n;
     }
     int inc = loc;
@@ -100,7 +107,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) voi
     for (int w = 0; w < wave; ++w) run += s_wtot[w];
     for (int b = b0; b < b1; ++b) {
       int p, lo, fp, n;
-      window_pages(ctx_lens[b], max_pages, window, p, lo, fp, n);
+      window_of(s_ctx[b], window, p, lo, fp, n);
       s_pre[b] = run * n_kv;
       run += n;
     }
@@ -113,160 +120,201 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) voi
   const int64_t page_stride = 2 * (int64_t)n_kv * BLK;
   const int64_t v_off = (int64_t)n_kv * BLK;
 
-  for (int r = blockIdx.x * 4 + wave; (int64_t)r * S < total; r += n_waves) {
-    int u = r * S;
-    const int u_end = min(total, u + S);
-    // sequence holding unit u: the last b with s_pre[b] <= u (non-empty, as s_pre[b + 1] > u)
-    int b = 0;
-    {
-      int hi = B;  // s_pre[hi] > u
-      while (hi - b > 1) {
-        const int mid = (b + hi) >> 1;
-        if (s_pre[mid] <= u) b = mid; else hi = mid;
-      }
+  // last b with s_pre[b] <= u (a non-empty sequence when u < total)
+  auto find_seq = [&](int u) {
+    int b = 0, hi = B;
+    while (hi - b > 1) {
+      const int mid = (b + hi) >> 1;
+      if (s_pre[mid] <= u) b = mid; else hi = mid;
     }
-    b = __builtin_amdgcn_readfirstlane(b);
-    while (u < u_end) {
-      while (__builtin_amdgcn_readfirstlane(s_pre[b + 1]) <= u) ++b;  // skip finished and empty sequences
-      const int base = __builtin_amdgcn_readfirstlane(s_pre[b]);
-      int p, lo, first_page, n_b;
-      window_pages(ctx_lens[b], max_pages, window, p, lo, first_page, n_b);
-      p = __builtin_amdgcn_readfirstlane(p);
-      lo = __builtin_amdgcn_readfirstlane(lo);
-      first_page = __builtin_amdgcn_readfirstlane(first_page);
-      n_b = __builtin_amdgcn_readfirstlane(n_b);
-      const int g = (u - base) / n_b;
-      const int s0 = base + g * n_b;          // first unit of sequence (b, g)
-      const int a = u - s0;                   // first window page of this segment
-      const int e = min(n_b, u_end - s0);     // one past its last
-      const int seq = b * n_kv + g;
-      const int first_r = s0 / S, n_seg = (s0 + n_b - 1) / S - first_r + 1;
-      u = s0 + e;
+    return b;
+  };
 
-      bf16x8 qf[KK];
-      {
-        const uint16_t *q = qkv + (int64_t)b * (n_q + 2 * n_kv) * D + (int64_t)(g * group + hl) * D;
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          u32x4 w = head_ok ? *(const u32x4 *)(q + kk * 32 + rq * 8) : u32x4{0u, 0u, 0u, 0u};
-          qf[kk] = __builtin_bit_cast(bf16x8, w);
-        }
+  for (int r = blockIdx.x * 4 + wave; (int64_t)r * S < total; r += n_waves) {
+    const int u0 = r * S, n_w = min(total, u0 + S) - u0;  // this range: units [u0, u0 + n_w)
+
+    // Page ids of range pages [t0, t0 + 64), one per lane (-1 past the range):
+    // each lane locates its own unit.
+    auto gather_ids = [&](int t0) {
+      const int t = t0 + lane;
+      if (t >= n_w) return -1;
+      const int u = u0 + t;
+      const int b = find_seq(u);
+      int p, lo, fp, n;
+      window_of(s_ctx[b], window, p, lo, fp, n);
+      const int page = (u - s_pre[b]) % n;
+      return page_table[(int64_t)b * max_pages + fp + page];
+    };
+
+    // ---- issue cursor: the next range page to load, as (sequence, head, window page)
+    int ib = __builtin_amdgcn_readfirstlane(find_seq(u0));
+    int ig, ipage, in_b, ifp, ilo, ip;
+    auto cursor_seq = [&]() {
+      int p, lo, fp, n;
+      window_of(s_ctx[ib], window, p, lo, fp, n);
+      ip = __builtin_amdgcn_readfirstlane(p);
+      ilo = __builtin_amdgcn_readfirstlane(lo);
+      ifp = __builtin_amdgcn_readfirstlane(fp);
+      in_b = __builtin_amdgcn_readfirstlane(n);
+    };
+    cursor_seq();
+    {
+      const int off = u0 - __builtin_amdgcn_readfirstlane(s_pre[ib]);
+      ig = off / in_b;
+      ipage = off % in_b;
+    }
+    int it = 0;  // range page index of the next issue
+    int ids_cur = gather_ids(0), ids_nxt = gather_ids(64);
+
+    // Issue the loads of the cursor's page into R and advance the cursor. Past
+    // the range the slot re-reads a valid page and is marked as padding, so the
+    // loads stay unconditional and the compiler can count them in flight.
+    auto issue = [&](PageRegs<D> &R) {
+      if (it > 0 && (it & 63) == 0) {
+        ids_cur = ids_nxt;
+        ids_nxt = gather_ids(it + 64);
       }
-      f32x4 acc[NB];
+      const bool live = it < n_w;
+      const int page = __builtin_amdgcn_readlane(ids_cur, it & 63);
+      R.seq = live ? ib * n_kv + ig : -1;
+      R.pg = ifp + ipage;
+      R.lo = ilo;
+      R.p = ip;
+      R.ok = live && (unsigned)page < (unsigned long long)pool_pages;
+      const uint16_t *kb = pool + (int64_t)ig * BLK + (int64_t)(R.ok ? page : 0) * page_stride;
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      float m_run = -INFINITY, l_run = 0.f;
-
-      const int32_t *pt = page_table + (int64_t)b * max_pages + first_page;
-      const uint16_t *pool_g = pool + (int64_t)g * BLK;
-      // page ids of window pages [c, c + 64) of the segment, one per lane (-1 past its end)
-      auto load_ids = [&](int c) { return (c + lane < e) ? pt[c + lane] : -1; };
-
-      auto consume = [&](PageRegs<D> &R) {
-        const int pg = R.pg;
-        const bool ok = R.ok;
-        f32x4 s = {0.f, 0.f, 0.f, 0.f};
+      for (int kk = 0; kk < KK; ++kk) R.k[kk] = *(const u32x4 *)(kb + hl * D + kk * 32 + rq * 8);
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) s = mfma_16x16x32(__builtin_bit_cast(bf16x8, R.k[kk]), qf[kk], s);
-        const int tok0 = pg * kPage + rq * 4;
-        const bool edge = !ok || (pg * kPage < lo) || (pg * kPage + kPage - 1 > p);
-        float sv[4];
+      for (int nb = 0; nb < NB; ++nb) R.v[nb] = *(const u32x2 *)(kb + v_off + (nb * 16 + hl) * kPage + rq * 4);
+      const uint16_t *qp = qkv + (int64_t)ib * row_elems + (int64_t)(ig * group + (head_ok ? hl : 0)) * D;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int t = tok0 + i;
-          sv[i] = (!edge || (ok && t >= lo && t <= p)) ? s[i] * scale_log2 : -INFINITY;
-        }
-        float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-        const float m_new = fmaxf(m_run, mx);
-        if (m_new == -INFINITY) return;  // only while every page so far had an invalid id
-        const float alpha = exp2f(m_run - m_new);  // m_run = -inf -> 0
-        float pv[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) pv[i] = exp2f(sv[i] - m_new);
-        l_run = l_run * alpha + ((pv[0] + pv[1]) + (pv[2] + pv[3]));
-        m_run = m_new;
-        bf16x4 pb;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) pb[i] = (__bf16)pv[i];
-        if (edge) {
-          // Zero the values of masked slots: their P is 0, but stale slots may
-          // hold non-finite bits and 0 * NaN would poison the accumulator.
-          const bool v0 = ok && tok0 >= lo && tok0 <= p, v1 = ok && tok0 + 1 >= lo && tok0 + 1 <= p;
-          const bool v2 = ok && tok0 + 2 >= lo && tok0 + 2 <= p, v3 = ok && tok0 + 3 >= lo && tok0 + 3 <= p;
-          const uint32_t m01 = (v0 ? 0xffffu : 0u) | (v1 ? 0xffff0000u : 0u);
-          const uint32_t m23 = (v2 ? 0xffffu : 0u) | (v3 ? 0xffff0000u : 0u);
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
-            R.v[nb][0] &= m01;
-            R.v[nb][1] &= m23;
+      for (int kk = 0; kk < KK; ++kk) R.q[kk] = *(const u32x4 *)(qp + kk * 32 + rq * 8);
+      if (live) {
+        ++it;
+        if (++ipage == in_b) {
+          ipage = 0;
+          if (++ig == n_kv) {
+            ig = 0;
+            if (it < n_w) {
+              ++ib;
+              while (__builtin_amdgcn_readfirstlane(s_pre[ib + 1]) == __builtin_amdgcn_readfirstlane(s_pre[ib])) ++ib;
+              cursor_seq();
+            }
           }
         }
+      }
+    };
+
+    // ---- consume side: the segment being accumulated
+    int cur_seq = -1, cur_first_pg = 0;
+    f32x4 acc[NB];
+    float m_run = -INFINITY, l_run = 0.f;
+    auto finish = [&]() {  // write the current segment's output or record
+      float l = l_run;
+      l += __shfl_xor(l, 16, kWave);
+      l += __shfl_xor(l, 32, kWave);
+      const int b = cur_seq / n_kv, g = cur_seq % n_kv;
+      const int n_b = (__builtin_amdgcn_readfirstlane(s_pre[b + 1]) - __builtin_amdgcn_readfirstlane(s_pre[b])) / n_kv;
+      const int s0 = __builtin_amdgcn_readfirstlane(s_pre[b]) + g * n_b;
+      const int first_r = s0 / S, n_seg = (s0 + n_b - 1) / S - first_r + 1;
+      int p, lo, fp, n;
+      window_of(s_ctx[b], window, p, lo, fp, n);
+      if (cur_first_pg == __builtin_amdgcn_readfirstlane(fp) && lane == 0)
+        ws_meta[cur_seq] = make_int2(first_r + cur_seq, n_seg);
+      if (!head_ok) return;
+      if (n_seg == 1) {
+        const float inv = l > 0.f ? 1.f / l : 0.f;
+        uint16_t *dst = o + ((int64_t)b * n_q + g * group + hl) * D;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          acc[nb] *= alpha;
-          acc[nb] = mfma_16x16x16(__builtin_bit_cast(bf16x4, R.v[nb]), pb, acc[nb]);
+          u32x2 w2;
+          w2[0] = pack2(acc[nb][0] * inv, acc[nb][1] * inv);
+          w2[1] = pack2(acc[nb][2] * inv, acc[nb][3] * inv);
+          *(u32x2 *)(dst + nb * 16 + rq * 4) = w2;
         }
-      };
-
-      int ids = load_ids(a);
-      for (int c0 = a; c0 < e; c0 += 64) {
-        const int n_my = min(64, e - c0);
-        const int ids_next = load_ids(c0 + 64);  // in flight while these 64 pages stream
-        // Issue the loads of page j of this batch (clamped to its last page so
-        // the loads are unconditional and the compiler can count them in flight).
-        auto issue = [&](PageRegs<D> &R, int j) {
-          const int jj = min(j, n_my - 1);
-          const int page = __builtin_amdgcn_readlane(ids, jj);
-          R.pg = first_page + c0 + j;
-          R.ok = (unsigned)page < (unsigned long long)pool_pages;
-          const uint16_t *kb = pool_g + (int64_t)(R.ok ? page : 0) * page_stride;
+      } else {
+        // record r + seq is unique: the sequences one range meets are consecutive
+        const int64_t rec = (int64_t)(r + cur_seq) * group + hl;
+        float *dst = ws_acc + rec * D;
 #pragma unroll
-          for (int kk = 0; kk < KK; ++kk) R.k[kk] = *(const u32x4 *)(kb + hl * D + kk * 32 + rq * 8);
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            R.v[nb] = *(const u32x2 *)(kb + v_off + (nb * 16 + hl) * kPage + rq * 4);
-        };
-        PageRegs<D> R0, R1;
-        issue(R0, 0);
-        issue(R1, 1);
-        for (int j = 0; j < n_my; j += 2) {
-          consume(R0);
-          issue(R0, j + 2);
-          if (j + 1 < n_my) consume(R1);
-          issue(R1, j + 3);
-        }
-        ids = ids_next;
-      }
-
-      l_run += __shfl_xor(l_run, 16, kWave);
-      l_run += __shfl_xor(l_run, 32, kWave);
-      if (a == 0 && lane == 0) ws_meta[seq] = make_int2(first_r + seq, n_seg);
-      if (head_ok) {
-        if (n_seg == 1) {
-          const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-          uint16_t *dst = o + ((int64_t)b * n_q + g * group + hl) * D;
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
-            u32x2 w2;
-            w2[0] = pack2(acc[nb][0] * inv, acc[nb][1] * inv);
-            w2[1] = pack2(acc[nb][2] * inv, acc[nb][3] * inv);
-            *(u32x2 *)(dst + nb * 16 + rq * 4) = w2;
-          }
-        } else {
-          // record r + seq is unique: sequences met by one range are consecutive
-          const int64_t rec = (int64_t)(r + seq) * group + hl;
-          float *dst = ws_acc + rec * D;
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) *(f32x4 *)(dst + nb * 16 + rq * 4) = acc[nb];
-          if (rq == 0) {
-            ws_ml[rec * 2] = m_run;
-            ws_ml[rec * 2 + 1] = l_run;
-          }
+        for (int nb = 0; nb < NB; ++nb) *(f32x4 *)(dst + nb * 16 + rq * 4) = acc[nb];
+        if (rq == 0) {
+          ws_ml[rec * 2] = m_run;
+          ws_ml[rec * 2 + 1] = l;
         }
       }
+    };
+
+    auto consume = [&](PageRegs<D> &R) {
+      if (R.seq != cur_seq) {  // uniform: the page opens a new segment
+        if (cur_seq >= 0) finish();
+        cur_seq = R.seq;
+        cur_first_pg = R.pg;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        m_run = -INFINITY;
+        l_run = 0.f;
+      }
+      const int pg = R.pg, lo = R.lo, p = R.p;
+      const bool ok = R.ok;
+      f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk)
+        s = mfma_16x16x32(__builtin_bit_cast(bf16x8, R.k[kk]), __builtin_bit_cast(bf16x8, R.q[kk]), s);
+      const int tok0 = pg * kPage + rq * 4;
+      const bool edge = !ok || (pg * kPage < lo) || (pg * kPage + kPage - 1 > p);
+      float sv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = tok0 + i;
+        sv[i] = (!edge || (ok && t >= lo && t <= p)) ? s[i] * scale_log2 : -INFINITY;
+      }
+      float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      const float m_new = fmaxf(m_run, mx);
+      if (m_new == -INFINITY) return;  // only while every page so far had an invalid id
+      const float alpha = exp2f(m_run - m_new);  // m_run = -inf -> 0
+      float pv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pv[i] = exp2f(sv[i] - m_new);
+      l_run = l_run * alpha + ((pv[0] + pv[1]) + (pv[2] + pv[3]));
+      m_run = m_new;
+      bf16x4 pb;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pb[i] = (__bf16)pv[i];
+      if (edge) {
+        // Zero the values of masked slots: their P is 0, but stale slots may
+        // hold non-finite bits and 0 * NaN would poison the accumulator.
+        const bool v0 = ok && tok0 >= lo && tok0 <= p, v1 = ok && tok0 + 1 >= lo && tok0 + 1 <= p;
+        const bool v2 = ok && tok0 + 2 >= lo && tok0 + 2 <= p, v3 = ok && tok0 + 3 >= lo && tok0 + 3 <= p;
+        const uint32_t m01 = (v0 ? 0xffffu : 0u) | (v1 ? 0xffff0000u : 0u);
+        const uint32_t m23 = (v2 ? 0xffffu : 0u) | (v3 ? 0xffff0000u : 0u);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          R.v[nb][0] &= m01;
+          R.v[nb][1] &= m23;
+        }
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        acc[nb] *= alpha;
+        acc[nb] = mfma_16x16x16(__builtin_bit_cast(bf16x4, R.v[nb]), pb, acc[nb]);
+      }
+    };
+
+    // Two pages in flight: while one is consumed the next is loading; the
+    // stream runs across segment boundaries without draining.
+    PageRegs<D> R0, R1;
+    issue(R0);
+    issue(R1);
+    for (int t = 0; t < n_w; t += 2) {
+      consume(R0);
+      issue(R0);
+      if (t + 1 < n_w) consume(R1);
+      issue(R1);
     }
+    finish();
   }
 }
 
@@ -384,7 +432,7 @@ hipError_t launch_attention(const uint16_t *qkv, int B, int n_q, int n_kv, int D
   float *ws_acc = ws;  // [records][group][D], 16-byte aligned rows
   float *ws_ml = ws_acc + (size_t)plan.records * group * D;
   int2 *ws_meta = (int2 *)(ws_ml + (size_t)plan.records * group * 2);
-  const size_t lds = ((size_t)B + 1) * sizeof(int);
+  const size_t lds = (2 * (size_t)B + 1) * sizeof(int);
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
   const dim3 mgrid((unsigned)(((int64_t)B * n_q + 3) / 4));
   auto go = [&](auto kflat, auto kmerge) {

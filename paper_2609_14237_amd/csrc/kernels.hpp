@@ -45,7 +45,7 @@ hipError_t launch_rope_append(uint16_t *qkv, int B, int n_q, int n_kv, int D, fl
 
 // Paged GQA decode attention (the batch's pages split evenly over the waves)
 // + exact log-sum-exp merge of sequences that span several waves.
-constexpr int kMaxAttnBatch = 8192;  // the kernel keeps a per-sequence prefix in LDS
+constexpr int kMaxAttnBatch = 4096;  // the kernel keeps per-sequence contexts and a prefix in LDS
 struct AttnPlan {
   int seg_pages;    // pages per wave range; 0: total / waves (at least 8)
   int grid;         // workgroups of the attention kernel

@@ -149,3 +149,16 @@ def test_buffer_sizes():
     assert B.ods_live_bytes(blk.c, n, B.BUFFERS.index("gu")) == 0
     cfg = R.layer_cfg(W.DENSE_8B_B64.layers[0])
     assert B.ods_kv_pool_bytes(cfg, 10) == 10 * 2 * 8 * 16 * 128 * 2
+
+
+def test_bench_handoff_bytes_match_the_live_set_table():
+    """Live-set bytes per token at each cut of the dense 8B-shaped layer: the
+    residual stream (8 KiB) plus what later operators of the layer still read."""
+    import bench
+    t = bench.handoff_bytes_per_token(W.BY_NAME["dense8b_b64"].layers[0])
+    KiB = 1024
+    assert [t[str(j)] for j in range(10)] == [16 * KiB, 20 * KiB, 20 * KiB, 16 * KiB, 16 * KiB, 8 * KiB,
+                                              16 * KiB, 64 * KiB, 36 * KiB, 8 * KiB]
+    m = bench.handoff_bytes_per_token(W.BY_NAME["moe64x8_b512"].layers[0])
+    assert len(m) == 14 and m["5"] == m["13"] == 8 * KiB
+    assert m["9"] == 8 * KiB + 8 * 8 * KiB + 64  # xp rows of the k = 8 slots, routing weights and slots
