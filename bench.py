@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--copies", type=int, default=0, help="weight/KV copies in rotation (0: auto)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work to time")
+    ap.add_argument("--ffn-sweep", action="store_true",
+                    help="instead of the decode step, time the dense FFN stage alone over batch sizes "
+                         "64..2048 to show where the GEMMs turn from HBM- to MFMA-bound")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the timed loop, run one plain device copy of this many MiB (a known-size "
                          "reference for hardware byte counters)")
@@ -166,12 +169,74 @@ def cpu_baseline(w, copy0, budget_s):
 
 # ----------------------------------------------------------------------------- main
 
+def ffn_sweep(args):
+    """Dense FFN stage ([6,10) of the 8B-shaped layer) at growing batch: the
+    weights stream once per call, so the GEMMs are HBM-bound at small batch and
+    turn MFMA-bound near the ridge (312 flop per byte at the vendor peaks)."""
+    import torch
+    import workloads as W
+    from workloads import gen
+    from paper_2609_14237_amd import binding as B
+    from paper_2609_14237_amd import runtime as R
+
+    base = W.BY_NAME["dense8b_b64"]
+    cfg = base.layers[0]
+    dev = "cuda"
+    torch.cuda.set_device(0)
+    copies = 3  # 3 x 352 MB of FFN weights defeat the 256 MB last-level cache
+    rows = []
+    for M in (64, 256, 512, 1024, 2048):
+        ctx = np.ones(M, dtype=np.int32)
+        page_table = np.zeros((M, 1), dtype=np.int32)
+        assert B.ods_kv_alloc(M, ctx, M, 0, 1, page_table) == 0, B.ods_last_error()
+        batch = R.DeviceBatch(torch.from_numpy(ctx).to(dev), torch.from_numpy(page_table).to(dev))
+        sets = []
+        for c in range(copies):
+            wts = [gen.layer_weights(cfg, base.seed + 1000 * c, 0, dev, base.router_std)]
+            pools = [gen.kv_pool(cfg, M, base.seed + 1000 * c, 0, dev)]
+            blk = R.DeviceBlock([cfg], wts, pools, M)
+            st = R.DeviceState(blk, batch, dev)
+            st.view("resid", M, cfg.hidden).copy_(gen.activations(M, cfg.hidden, base.seed + c, dev))
+            sets.append((blk, st, wts, pools))
+        stream = torch.cuda.current_stream().cuda_stream
+        for i in range(args.warmup):
+            blk, st = sets[i % copies][:2]
+            R.run_partition(blk, 6, 10, batch, st, stream)
+        torch.cuda.synchronize()
+        times = []
+        for i in range(args.steps):
+            blk, st = sets[i % copies][:2]
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            R.run_partition(blk, 6, 10, batch, st, stream)
+            e1.record()
+            times.append((e0, e1))
+        torch.cuda.synchronize()
+        t = float(np.median([a.elapsed_time(b) for a, b in times])) * 1e-3
+        F, H = cfg.ffn, cfg.hidden
+        nbytes, flops = 6 * H * F + 4 * M * H, 6 * M * H * F
+        rows.append({"batch": M, "us": t * 1e6, "tokens_per_s": M / t, "hbm_GBps": nbytes / t / 1e9,
+                     "hbm_frac": nbytes / t / HBM_PEAK, "mfma_TFLOPs": flops / t / 1e12,
+                     "mfma_frac": flops / t / MFMA_BF16_PEAK,
+                     "roofline_us": max(nbytes / HBM_PEAK, flops / MFMA_BF16_PEAK) * 1e6,
+                     "bound": "mfma" if flops / MFMA_BF16_PEAK > nbytes / HBM_PEAK else "hbm"})
+        print(f"[ffn-sweep] batch {M}: {t * 1e6:.1f} us, {flops / t / 1e12:.0f} TFLOP/s", file=sys.stderr, flush=True)
+        del sets
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": "dense FFN stage time vs batch (8B-shaped layer)", "unit": "us",
+                      "steps": args.steps, "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
+                      "ffn_sweep": rows}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(collectives and sharding are out of scope); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.ffn_sweep:
+        ffn_sweep(args)
+        return
 
     import torch
     import workloads as W
