@@ -43,6 +43,10 @@ def parse():
     ap.add_argument("--ffn-sweep", action="store_true",
                     help="instead of the decode step, time the dense FFN stage alone over batch sizes "
                          "64..2048 to show where the GEMMs turn from HBM- to MFMA-bound")
+    ap.add_argument("--latency-table", action="store_true",
+                    help="instead of the decode step, time the stage templates (attention, FFN, core "
+                         "attention, colocated layer) over batch and context sweeps, as HIP-graph replays "
+                         "and as eager calls")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the timed loop, run one plain device copy of this many MiB (a known-size "
                          "reference for hardware byte counters)")
@@ -228,6 +232,72 @@ def ffn_sweep(args):
                       "ffn_sweep": rows}), flush=True)
 
 
+def latency_table(args):
+    """Profiled stage latencies t_j = f_lat(op range, batch, context), the
+    per-stage inputs of the paper's communication-aware latency model (Section
+    4), for the dense 8B-shaped layer: every stage template at every (batch,
+    context) point, timed as a replay of its captured HIP graph and as an
+    eager ods_run_partition call (median of --steps each). One weight/KV copy:
+    small KV footprints partly stay in the 256 MB last-level cache."""
+    import torch
+    import workloads as W
+    from workloads import gen
+    from paper_2609_14237_amd import binding as B
+    from paper_2609_14237_amd import runtime as R
+
+    base = W.BY_NAME["dense8b_b64"]
+    cfg = base.layers[0]
+    dev = "cuda"
+    torch.cuda.set_device(0)
+    templates = [("attention stage", 0, 6), ("FFN stage", 6, 10), ("core attention", 3, 5), ("colocated layer", 0, 10)]
+    weights = [gen.layer_weights(cfg, base.seed, 0, dev, base.router_std)]
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def median_us(fn):
+        for _ in range(args.warmup):
+            fn()
+        evs = []
+        for _ in range(args.steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            evs.append((e0, e1))
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in evs])) * 1e3
+
+    rows = []
+    for ctx_len in (1024, 4096, 16384):
+        for M in (1, 8, 32, 64, 128, 256):
+            ctx = np.full(M, ctx_len, dtype=np.int32)
+            P = gen.pool_pages_for(ctx)
+            max_pages = -(-ctx_len // 16)
+            table = np.zeros((M, max_pages), dtype=np.int32)
+            assert B.ods_kv_alloc(P, ctx, M, base.seed, max_pages, table) == 0, B.ods_last_error()
+            batch = R.DeviceBatch(torch.from_numpy(ctx).to(dev), torch.from_numpy(table).to(dev))
+            pools = [gen.kv_pool(cfg, P, base.seed, 0, dev)]
+            blk = R.DeviceBlock([cfg], weights, pools, P)
+            st = R.DeviceState(blk, batch, dev)
+            x = gen.activations(M, cfg.hidden, base.seed, dev)
+            for name, a, b in templates:
+                st.view("resid", M, cfg.hidden).copy_(x)
+                if a > 0:  # inputs of a later stage: run the layer up to it once
+                    R.run_partition(blk, 0, a, batch, st, stream)
+                t_eager = median_us(lambda: R.run_partition(blk, a, b, batch, st, stream))
+                g = R.PartitionGraph(blk, a, b, batch, st)
+                t_graph = median_us(lambda: g.launch(stream))
+                g.close()
+                rows.append({"stage": name, "op_range": [a, b], "batch": M, "ctx": ctx_len,
+                             "us_graph": t_graph, "us_eager": t_eager})
+                print(f"[latency] ctx {ctx_len} batch {M} {name} [{a},{b}): graph {t_graph:.1f} us, "
+                      f"eager {t_eager:.1f} us", file=sys.stderr, flush=True)
+            del blk, st, pools, batch
+            torch.cuda.empty_cache()
+    print(json.dumps({"metric": "stage latency t_j = f_lat(op range, batch, context), dense 8B-shaped layer",
+                      "unit": "us", "steps": args.steps, "warmup": args.warmup, "dtype": "bf16",
+                      "data": "synthetic", "latency_table": rows}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -236,6 +306,9 @@ def main():
         sys.exit(2)
     if args.ffn_sweep:
         ffn_sweep(args)
+        return
+    if args.latency_table:
+        latency_table(args)
         return
 
     import torch

@@ -203,6 +203,26 @@ ods_status ods_attn_stage(const ods_block *blk, int32_t layer, const ods_batch *
 ods_status ods_ffn_stage(const ods_block *blk, int32_t layer, const ods_batch *batch,
                          ods_state *state, hipStream_t stream);
 
+/* Capture operators [op_begin, op_end) as an instantiated HIP graph, so a
+ * stage replays as one submission with its buffers bound once (Section 6:
+ * static plan capacity; graphs and buffers bound once, only token, position
+ * and KV metadata change between iterations).
+ * The graph holds the pointers of blk, batch and state and the host values
+ * they carry (batch size, max_pages, split_pages, shapes) as of this call; the
+ * device contents they point to (resid, ctx_lens, page_table, weights, pools)
+ * are read at each launch, so a new decode step only rewrites those buffers.
+ * Validation is that of ods_run_partition; on a non-OK status *exec is NULL.
+ * The caller owns *exec: launch it with ods_graph_launch, free it with
+ * ods_graph_destroy. Capture runs on a private stream and enqueues nothing. */
+ods_status ods_partition_graph(const ods_block *blk, int32_t op_begin, int32_t op_end,
+                               const ods_batch *batch, ods_state *state, hipGraphExec_t *exec);
+
+/* Launch a graph from ods_partition_graph on `stream` (hipGraphLaunch). */
+ods_status ods_graph_launch(hipGraphExec_t exec, hipStream_t stream);
+
+/* Free a graph from ods_partition_graph (NULL is a no-op). */
+ods_status ods_graph_destroy(hipGraphExec_t exec);
+
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char *ods_last_error(void);
 

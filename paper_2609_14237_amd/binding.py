@@ -68,6 +68,10 @@ SIGNATURES = {
                                  C.POINTER(ods_state), C.c_void_p]),
     "ods_ffn_stage": (C.c_int, [C.POINTER(ods_block), C.c_int32, C.POINTER(ods_batch),
                                 C.POINTER(ods_state), C.c_void_p]),
+    "ods_partition_graph": (C.c_int, [C.POINTER(ods_block), C.c_int32, C.c_int32, C.POINTER(ods_batch),
+                                      C.POINTER(ods_state), C.POINTER(C.c_void_p)]),
+    "ods_graph_launch": (C.c_int, [C.c_void_p, C.c_void_p]),
+    "ods_graph_destroy": (C.c_int, [C.c_void_p]),
     "ods_last_error": (C.c_char_p, []),
 }
 
@@ -144,3 +148,18 @@ def ods_ffn_stage(blk: ods_block, layer: int, batch: ods_batch, state: ods_state
 
 def ods_last_error() -> str:
     return lib.ods_last_error().decode()
+
+
+def ods_partition_graph(blk: ods_block, op_begin: int, op_end: int, batch: ods_batch, state: ods_state):
+    """(status, exec handle or None)."""
+    h = C.c_void_p()
+    st = lib.ods_partition_graph(C.byref(blk), op_begin, op_end, C.byref(batch), C.byref(state), C.byref(h))
+    return st, h.value
+
+
+def ods_graph_launch(exec_handle: int, stream: int) -> int:
+    return lib.ods_graph_launch(exec_handle, stream)
+
+
+def ods_graph_destroy(exec_handle) -> int:
+    return lib.ods_graph_destroy(exec_handle)

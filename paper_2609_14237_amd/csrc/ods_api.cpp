@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <string>
 #include <vector>
 
 #include "../../include/ods.h"
@@ -450,6 +451,54 @@ ods_status ods_ffn_stage(const ods_block *blk, int32_t layer, const ods_batch *b
   if (layer < 0 || layer >= blk->n_layers) return fail(ODS_ERANGE, "layer %d outside [0, %d)", layer, blk->n_layers);
   const int off = layer_offset(blk, layer);
   return ods_run_partition(blk, off + 6, off + layer_ops(blk->layers[layer].cfg), batch, state, stream);
+}
+
+ods_status ods_partition_graph(const ods_block *blk, int32_t op_begin, int32_t op_end, const ods_batch *batch,
+                               ods_state *state, hipGraphExec_t *exec) {
+  if (!exec) return fail(ODS_EINVAL, "exec is null");
+  *exec = nullptr;
+  hipStream_t s = nullptr;
+  hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+  if (e != hipSuccess) return fail(ODS_EHIP, "hipStreamCreate: %s", hipGetErrorString(e));
+  e = hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal);
+  if (e != hipSuccess) {
+    hipStreamDestroy(s);
+    return fail(ODS_EHIP, "hipStreamBeginCapture: %s", hipGetErrorString(e));
+  }
+  const ods_status rc = ods_run_partition(blk, op_begin, op_end, batch, state, s);
+  std::string msg = rc == ODS_OK ? "" : g_err;
+  hipGraph_t graph = nullptr;
+  e = hipStreamEndCapture(s, &graph);
+  hipStreamDestroy(s);
+  if (rc != ODS_OK) {
+    if (graph) hipGraphDestroy(graph);
+    return fail(rc, "%s", msg.c_str());
+  }
+  if (e != hipSuccess || !graph) return fail(ODS_EHIP, "hipStreamEndCapture: %s", hipGetErrorString(e));
+  e = hipGraphInstantiate(exec, graph, nullptr, nullptr, 0);
+  hipGraphDestroy(graph);
+  if (e != hipSuccess) {
+    *exec = nullptr;
+    return fail(ODS_EHIP, "hipGraphInstantiate: %s", hipGetErrorString(e));
+  }
+  g_err[0] = 0;
+  return ODS_OK;
+}
+
+ods_status ods_graph_launch(hipGraphExec_t exec, hipStream_t stream) {
+  if (!exec) return fail(ODS_EINVAL, "exec is null");
+  const hipError_t e = hipGraphLaunch(exec, stream);
+  if (e != hipSuccess) return fail(ODS_EHIP, "hipGraphLaunch: %s", hipGetErrorString(e));
+  g_err[0] = 0;
+  return ODS_OK;
+}
+
+ods_status ods_graph_destroy(hipGraphExec_t exec) {
+  if (!exec) return ODS_OK;
+  const hipError_t e = hipGraphExecDestroy(exec);
+  if (e != hipSuccess) return fail(ODS_EHIP, "hipGraphExecDestroy: %s", hipGetErrorString(e));
+  g_err[0] = 0;
+  return ODS_OK;
 }
 
 }  // extern "C"

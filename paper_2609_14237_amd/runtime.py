@@ -120,3 +120,30 @@ def attn_stage(block, layer, batch, state, stream=None) -> None:
 def ffn_stage(block, layer, batch, state, stream=None) -> None:
     st = _b.ods_ffn_stage(block.c, layer, batch.c, state.c, current_stream() if stream is None else stream)
     _b._check(st, f"ods_ffn_stage({layer})")
+
+
+class PartitionGraph:
+    """Operators [op_begin, op_end) captured once as a HIP graph; launch()
+    replays them on a stream with the buffers bound at capture. Rewrite the
+    device contents (resid, ctx_lens, page_table) between launches; keep the
+    block, batch and state objects (and their buffers) alive while the graph is."""
+
+    def __init__(self, block: DeviceBlock, op_begin: int, op_end: int, batch: DeviceBatch, state: DeviceState):
+        st, h = _b.ods_partition_graph(block.c, op_begin, op_end, batch.c, state.c)
+        _b._check(st, f"ods_partition_graph[{op_begin},{op_end})")
+        self.handle = h
+        self._keep = (block, batch, state)
+
+    def launch(self, stream: int | None = None) -> None:
+        _b._check(_b.ods_graph_launch(self.handle, current_stream() if stream is None else stream), "ods_graph_launch")
+
+    def close(self) -> None:
+        if self.handle:
+            _b.ods_graph_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

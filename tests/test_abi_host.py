@@ -162,3 +162,11 @@ def test_bench_handoff_bytes_match_the_live_set_table():
     m = bench.handoff_bytes_per_token(W.BY_NAME["moe64x8_b512"].layers[0])
     assert len(m) == 14 and m["5"] == m["13"] == 8 * KiB
     assert m["9"] == 8 * KiB + 8 * 8 * KiB + 64  # xp rows of the k = 8 slots, routing weights and slots
+
+
+def test_graph_entry_points_reject_null_handles():
+    blk = fake_block(W.TINY.layers)
+    batch, state = fake_batch(), fake_state()
+    assert B.lib.ods_partition_graph(C.byref(blk.c), 0, 1, C.byref(batch), C.byref(state), None) == B.ODS_EINVAL
+    assert B.ods_graph_launch(None, 0) == B.ODS_EINVAL
+    assert B.ods_graph_destroy(None) == B.ODS_OK
