@@ -83,24 +83,10 @@ def layer_accounting(cfg, ctx, B):
 
 
 def handoff_bytes_per_token(cfg):
-    """Bytes per decoded token of the live set that crosses a cut after each
-    local operator of a layer (the activation interface between two stages):
-    the residual stream plus whatever later operators of the layer still read.
-    Per-batch items (expert_off) are left out."""
-    H, nq, nkv, d = cfg.hidden, cfg.n_q, cfg.n_kv, cfg.head_dim
-    resid, qkv, q, o = 2 * H, 2 * cfg.qkv_dim, 2 * nq * d, 2 * nq * d
-    if not cfg.n_experts:
-        F = cfg.ffn
-        live = [resid + 2 * H, resid + qkv, resid + qkv, resid + q, resid + o, resid,
-                resid + 2 * H, resid + 4 * F, resid + 2 * F, resid]
-    else:
-        E, k, I = cfg.n_experts, cfg.top_k, cfg.moe_ffn
-        route = 4 * k + 4 * k  # topk_w and slot_pos, read by the combine
-        live = [resid + 2 * H, resid + qkv, resid + qkv, resid + q, resid + o, resid,
-                resid + 2 * H, resid + 2 * H + 4 * E, resid + 2 * H + 8 * k,
-                resid + 2 * k * H + route, resid + 4 * k * I + route, resid + 2 * k * I + route,
-                resid + 2 * k * H + route, resid]
-    return {str(j): int(b) for j, b in enumerate(live)}
+    """Bytes per decoded token of the live set crossing a cut after each local
+    operator of a layer, keyed by the operator index as a string."""
+    from paper_2609_14237_amd.costmodel import handoff_bytes_per_token as live
+    return {str(j): int(b) for j, b in enumerate(live(cfg))}
 
 
 def attn_source_hash():
@@ -266,7 +252,7 @@ def latency_table(args):
         torch.cuda.synchronize()
         return float(np.median([a.elapsed_time(b) for a, b in evs])) * 1e3
 
-    rows = []
+    rows, op_rows = [], []
     for ctx_len in (1024, 4096, 16384):
         for M in (1, 8, 32, 64, 128, 256):
             ctx = np.full(M, ctx_len, dtype=np.int32)
@@ -279,6 +265,12 @@ def latency_table(args):
             blk = R.DeviceBlock([cfg], weights, pools, P)
             st = R.DeviceState(blk, batch, dev)
             x = gen.activations(M, cfg.hidden, base.seed, dev)
+            for i in range(10):  # single operators, eager, for per-operator latency models
+                st.view("resid", M, cfg.hidden).copy_(x)
+                if i > 0:
+                    R.run_partition(blk, 0, i, batch, st, stream)
+                t_op = median_us(lambda: R.run_partition(blk, i, i + 1, batch, st, stream))
+                op_rows.append({"local": i, "name": blk.op_name(i), "batch": M, "ctx": ctx_len, "us": t_op})
             for name, a, b in templates:
                 st.view("resid", M, cfg.hidden).copy_(x)
                 if a > 0:  # inputs of a later stage: run the layer up to it once
@@ -295,7 +287,7 @@ def latency_table(args):
             torch.cuda.empty_cache()
     print(json.dumps({"metric": "stage latency t_j = f_lat(op range, batch, context), dense 8B-shaped layer",
                       "unit": "us", "steps": args.steps, "warmup": args.warmup, "dtype": "bf16",
-                      "data": "synthetic", "latency_table": rows}), flush=True)
+                      "data": "synthetic", "latency_table": rows, "op_latency": op_rows}), flush=True)
 
 
 def main():

@@ -1,0 +1,491 @@
+"""Analytical cost model and a small exhaustive serving planner (host side, no GPU).
+
+Cost model (Section 3 and Appendix A). A GPU type is (c, beta, M, F): unit-time
+price, memory bandwidth, memory capacity, peak compute. With alpha = c / beta
+(price per byte moved) and gamma = c / F (price per flop), the per-token cost
+of decoding at average sequence length s is
+  homogeneous disaggregation   CPT_hom(s)   = alpha m_kv(s) + 2 gamma P_act
+  heterogeneous (attn on j,
+    GEMM operators on k)       CPT_het(s)   = alpha_j m_kv(s) + 2 gamma_k P_act
+  colocated                    CPT_coloc(s) = alpha m_kv(s)
+                                              + max(alpha M_weights / b_bar(s), 2 gamma P_act)
+with b_bar(s) = (M - M_weights) / m_kv(s) the relaxed feasible batch and
+b_max = floor(b_bar). GEMMs turn compute-bound at b* = M_weights F / (2 P_act beta).
+Theorem 1 bounds the gain G_hom = CPT_coloc / CPT_hom by M / (M - M_weights);
+Theorem 2 bounds G_het = min_j CPT_hom_j / CPT_het_* by (1 + sqrt(eta)) / 2 with
+eta = beta_1 F_2 / (beta_2 F_1) >= 1, and puts its peak at the crossing
+x* = 2 P_act (gamma_1 - gamma_2) / (alpha_2 - alpha_1) of x = m_kv(s).
+
+Planner (Sections 4-5, Appendix B). A partition block of N ordered operators
+is cut by a contiguous template q = (0 = q_0 < ... < q_S = N); stage j runs on
+owner sigma(j) = ((j - 1) mod K) + 1 (here K = S, one stage position per
+owner). Stage latency t_j sums its operators' latencies at the per-replica
+microbatch b_hat (roofline estimates max(D / beta, W / F), or measured
+per-operator profiles); the transfer after stage j moves the live set at that
+cut, u_j = b_hat * A_j / link bandwidth. The round-trip time of mu
+microbatches over B_total blocks is taken as the larger of the two lower
+bounds the paper's branch-and-bound uses: the dependency chain of one
+microbatch, B_total * sum_j (t_j + u_j) (the last block's wrap-around transfer
+omitted), and the serialized work of the busiest resource, mu * B_total *
+t_j per owner and per link. A plan costs CPT = T_rtt * sum_m c_m / b_m with
+b_m = mu * b_hat, subject to T_rtt <= SLO and, per owner, weights of its
+stages plus the KV of mu resident microbatches within M. The search is
+exhaustive over S, templates (and the block's rotation, so a stage may wrap
+the block boundary as CAD's rest-of-model stage does), mu and b_hat.
+"""
+from __future__ import annotations
+
+import bisect
+import itertools
+import math
+from dataclasses import dataclass, field
+from typing import Callable, Sequence
+
+BF16 = 2  # bytes per weight / activation element
+
+
+# ---------------------------------------------------------------- hardware and model
+
+@dataclass(frozen=True)
+class Gpu:
+    name: str
+    price_per_hour: float   # c, USD per GPU-hour
+    bandwidth: float        # beta, bytes / s
+    memory: float           # M, bytes
+    flops: float            # F, bf16 flop / s (dense)
+
+    @property
+    def c(self) -> float:
+        """Unit-time cost, USD per second."""
+        return self.price_per_hour / 3600.0
+
+    @property
+    def alpha(self) -> float:
+        return self.c / self.bandwidth
+
+    @property
+    def gamma(self) -> float:
+        return self.c / self.flops
+
+
+MI355X = Gpu("MI355X", price_per_hour=1.0, bandwidth=8.0e12, memory=288e9, flops=2.5166e15)
+
+
+def _is_moe(cfg) -> bool:
+    return bool(getattr(cfg, "n_experts", 0))
+
+
+def layer_weight_params(cfg) -> int:
+    """Resident GEMM parameters of one layer (all experts for MoE)."""
+    H, d = cfg.hidden, cfg.head_dim
+    attn = cfg.qkv_dim * H + H * cfg.n_q * d
+    if _is_moe(cfg):
+        return attn + cfg.n_experts * 3 * H * cfg.moe_ffn + H * cfg.n_experts
+    return attn + 3 * H * cfg.ffn
+
+
+def layer_active_params(cfg) -> int:
+    """GEMM parameters one token activates in one layer (top-k experts for MoE)."""
+    H, d = cfg.hidden, cfg.head_dim
+    attn = cfg.qkv_dim * H + H * cfg.n_q * d
+    if _is_moe(cfg):
+        return attn + cfg.top_k * 3 * H * cfg.moe_ffn + H * cfg.n_experts
+    return attn + 3 * H * cfg.ffn
+
+
+def layer_kv_bytes(cfg, s: float) -> float:
+    """KV-cache bytes one request keeps in this layer at sequence length s
+    (a sliding-window layer keeps at most its window)."""
+    tokens = min(s, cfg.window) if getattr(cfg, "window", 0) else s
+    return 2 * cfg.n_kv * cfg.head_dim * BF16 * tokens
+
+
+@dataclass(frozen=True)
+class Model:
+    """A model as B_total repeats of a partition block of layers."""
+    block: tuple
+    n_blocks: int
+
+    @property
+    def p_act(self) -> float:
+        return self.n_blocks * sum(layer_active_params(c) for c in self.block)
+
+    @property
+    def m_weights(self) -> float:
+        return self.n_blocks * sum(layer_weight_params(c) for c in self.block) * BF16
+
+    def m_kv(self, s: float) -> float:
+        return self.n_blocks * sum(layer_kv_bytes(c, s) for c in self.block)
+
+
+# ---------------------------------------------------------------- Section 3 closed forms
+
+def cpt_hom(g: Gpu, m: Model, s: float) -> float:
+    return g.alpha * m.m_kv(s) + 2 * g.gamma * m.p_act
+
+
+def cpt_het(g_attn: Gpu, g_gemm: Gpu, m: Model, s: float) -> float:
+    return g_attn.alpha * m.m_kv(s) + 2 * g_gemm.gamma * m.p_act
+
+
+def b_bar(g: Gpu, m: Model, s: float) -> float:
+    return (g.memory - m.m_weights) / m.m_kv(s)
+
+
+def b_max(g: Gpu, m: Model, s: float) -> int:
+    return math.floor(b_bar(g, m, s))
+
+
+def cpt_coloc(g: Gpu, m: Model, s: float) -> float:
+    bb = b_bar(g, m, s)
+    if bb < 1:
+        raise ValueError("colocation is infeasible at this sequence length (b_bar < 1)")
+    return g.alpha * m.m_kv(s) + max(g.alpha * m.m_weights / bb, 2 * g.gamma * m.p_act)
+
+
+def b_star(g: Gpu, m: Model) -> float:
+    """Batch at which GEMM weight-loading time equals compute time."""
+    return m.m_weights * g.flops / (2 * m.p_act * g.bandwidth)
+
+
+def g_hom(g: Gpu, m: Model, s: float) -> float:
+    return cpt_coloc(g, m, s) / cpt_hom(g, m, s)
+
+
+def g_hom_bound(g: Gpu, m: Model) -> float:
+    return g.memory / (g.memory - m.m_weights)
+
+
+def eta(g1: Gpu, g2: Gpu) -> float:
+    """Hardware ratio beta_1 F_2 / (beta_2 F_1), taken >= 1 by labelling."""
+    r = (g1.bandwidth * g2.flops) / (g2.bandwidth * g1.flops)
+    return max(r, 1.0 / r)
+
+
+def g_het(gpus: Sequence[Gpu], m: Model, s: float) -> float:
+    hom = min(cpt_hom(g, m, s) for g in gpus)
+    het = min(g.alpha for g in gpus) * m.m_kv(s) + min(g.gamma for g in gpus) * 2 * m.p_act
+    return hom / het
+
+
+def g_het_bound(e: float) -> float:
+    return (1.0 + math.sqrt(e)) / 2.0
+
+
+def x_star(g1: Gpu, g2: Gpu, m: Model) -> float:
+    """KV bytes per request at which the two homogeneous costs cross; the
+    types are labelled so that g1 is the cheaper one per byte."""
+    if g1.alpha > g2.alpha:
+        g1, g2 = g2, g1
+    return 2 * m.p_act * (g1.gamma - g2.gamma) / (g2.alpha - g1.alpha)
+
+
+# ---------------------------------------------------------------- operators of a block
+
+OP_NAMES_DENSE = ("attn_norm", "qkv_proj", "rope", "kv_append", "attn_core", "o_proj_residual",
+                  "ffn_norm", "gate_up", "silu_mul", "down_residual")
+OP_NAMES_MOE = OP_NAMES_DENSE[:7] + ("router", "topk_softmax", "moe_permute", "expert_gate_up", "silu_mul",
+                                     "expert_down", "moe_combine_residual")
+
+
+def layer_op_names(cfg) -> tuple:
+    return OP_NAMES_MOE if _is_moe(cfg) else OP_NAMES_DENSE
+
+
+def handoff_bytes_per_token(cfg) -> list:
+    """Bytes per request of the live set that crosses a cut after each local
+    operator of a layer (the activation interface A_j): the residual stream
+    plus whatever later operators of the layer still read."""
+    H, nq, d = cfg.hidden, cfg.n_q, cfg.head_dim
+    resid, qkv, q, o = 2 * H, 2 * cfg.qkv_dim, 2 * nq * d, 2 * nq * d
+    if not _is_moe(cfg):
+        F = cfg.ffn
+        return [resid + 2 * H, resid + qkv, resid + qkv, resid + q, resid + o, resid,
+                resid + 2 * H, resid + 4 * F, resid + 2 * F, resid]
+    E, k, I = cfg.n_experts, cfg.top_k, cfg.moe_ffn
+    route = 4 * k + 4 * k  # routing weights and slots, read by the combine
+    return [resid + 2 * H, resid + qkv, resid + qkv, resid + q, resid + o, resid,
+            resid + 2 * H, resid + 2 * H + 4 * E, resid + 2 * H + 8 * k,
+            resid + 2 * k * H + route, resid + 4 * k * I + route, resid + 2 * k * I + route,
+            resid + 2 * k * H + route, resid]
+
+
+def op_bytes_flops(cfg, op: str, b: float, s: float):
+    """(D, W, resident weight bytes, KV bytes per request) of one operator of a
+    layer at batch b and sequence length s, per the roofline accounting of
+    Appendix A (weights read once per call, activations in and out)."""
+    H, nq, nkv, d = cfg.hidden, cfg.n_q, cfg.n_kv, cfg.head_dim
+    qd = cfg.qkv_dim
+    if op in ("attn_norm", "ffn_norm"):
+        return 2 * BF16 * b * H, 4 * b * H, 0, 0
+    if op == "qkv_proj":
+        w = qd * H * BF16
+        return w + BF16 * b * (H + qd), 2 * b * H * qd, w, 0
+    if op == "rope":
+        return 2 * BF16 * b * (nq + nkv) * d, 6 * b * (nq + nkv) * d, 0, 0
+    if op == "kv_append":
+        return BF16 * b * 2 * nkv * d, 0, 0, 0
+    if op == "attn_core":
+        kv = layer_kv_bytes(cfg, s)
+        tokens = kv / (2 * nkv * d * BF16)
+        return b * kv + 2 * BF16 * b * nq * d, 4 * b * nq * d * tokens, 0, kv
+    if op == "o_proj_residual":
+        w = H * nq * d * BF16
+        return w + BF16 * b * (nq * d + 2 * H), 2 * b * H * nq * d, w, 0
+    if _is_moe(cfg):
+        E, k, I = cfg.n_experts, cfg.top_k, cfg.moe_ffn
+        touched = E * (1.0 - (1.0 - k / E) ** b)  # experts hit by at least one of b tokens
+        if op == "router":
+            w = E * H * BF16
+            return w + BF16 * b * H + 4 * b * E, 2 * b * H * E, w, 0
+        if op == "topk_softmax":
+            return 4 * b * E + 8 * b * k, 8 * b * E, 0, 0
+        if op == "moe_permute":
+            return 2 * BF16 * b * k * H, 0, 0, 0
+        if op == "expert_gate_up":
+            return touched * 2 * I * H * BF16 + BF16 * b * k * (H + 2 * I), 2 * b * k * H * 2 * I, E * 2 * I * H * BF16, 0
+        if op == "silu_mul":
+            return BF16 * b * k * 3 * I, 4 * b * k * I, 0, 0
+        if op == "expert_down":
+            return touched * H * I * BF16 + BF16 * b * k * (I + H), 2 * b * k * H * I, E * H * I * BF16, 0
+        if op == "moe_combine_residual":
+            return BF16 * b * (k * H + 2 * H) + 4 * b * k, 2 * b * k * H, 0, 0
+    else:
+        F = cfg.ffn
+        if op == "gate_up":
+            w = 2 * F * H * BF16
+            return w + BF16 * b * (H + 2 * F), 2 * b * H * 2 * F, w, 0
+        if op == "silu_mul":
+            return BF16 * b * 3 * F, 4 * b * F, 0, 0
+        if op == "down_residual":
+            w = H * F * BF16
+            return w + BF16 * b * (F + 2 * H), 2 * b * H * F, w, 0
+    raise ValueError(f"unknown operator {op}")
+
+
+@dataclass(frozen=True)
+class BlockOp:
+    layer: int
+    local: int
+    name: str
+    cfg: object
+
+
+def block_ops(block: Sequence) -> list:
+    return [BlockOp(l, j, n, c) for l, c in enumerate(block) for j, n in enumerate(layer_op_names(c))]
+
+
+def roofline_latency(g: Gpu) -> Callable:
+    """Operator latency max(D / beta, W / F) of Appendix A."""
+    def lat(op: BlockOp, b: float, s: float) -> float:
+        D, W, _, _ = op_bytes_flops(op.cfg, op.name, b, s)
+        return max(D / g.bandwidth, W / g.flops)
+    return lat
+
+
+class ProfiledLatency:
+    """Measured single-operator latencies t(op, b, s) of one layer shape,
+    interpolated linearly in batch and sequence length (clamped at the ends).
+    rows: iterable of dicts with keys local (operator index), batch, ctx, us."""
+
+    def __init__(self, rows):
+        table = {}
+        for r in rows:
+            table.setdefault(int(r["local"]), {}).setdefault(float(r["ctx"]), []).append((float(r["batch"]), float(r["us"])))
+        self.table = {j: {c: sorted(v) for c, v in per.items()} for j, per in table.items()}
+
+    @staticmethod
+    def _interp(pts, x):
+        xs = [p[0] for p in pts]
+        i = bisect.bisect_left(xs, x)
+        if i == 0:
+            return pts[0][1]
+        if i == len(pts):
+            return pts[-1][1]
+        (x0, y0), (x1, y1) = pts[i - 1], pts[i]
+        return y0 + (y1 - y0) * (x - x0) / (x1 - x0)
+
+    def __call__(self, op: BlockOp, b: float, s: float) -> float:
+        per = self.table[op.local]
+        ctxs = sorted(per)
+        i = bisect.bisect_left(ctxs, s)
+        if i == 0 or i == len(ctxs):
+            c = ctxs[0] if i == 0 else ctxs[-1]
+            return self._interp(per[c], b) * 1e-6
+        c0, c1 = ctxs[i - 1], ctxs[i]
+        y0, y1 = self._interp(per[c0], b), self._interp(per[c1], b)
+        return (y0 + (y1 - y0) * (s - c0) / (c1 - c0)) * 1e-6
+
+
+# ---------------------------------------------------------------- templates and plans
+
+def templates(n_ops: int, S: int):
+    """Every contiguous template q = (0, q_1, ..., q_{S-1}, n_ops)."""
+    for cut in itertools.combinations(range(1, n_ops), S - 1):
+        yield (0,) + cut + (n_ops,)
+
+
+def count_templates(n_ops: int, S: int) -> int:
+    return math.comb(n_ops - 1, S - 1)
+
+
+def subblock_templates(n_ops: int, n_rep: int, K: int):
+    """Templates chosen inside one of n_rep identical sub-blocks and tiled over
+    the block (S = n_rep * K stages)."""
+    if n_ops % n_rep:
+        raise ValueError("the sub-block must divide the block")
+    sub = n_ops // n_rep
+    for q in templates(sub, K):
+        out = [0]
+        for r in range(n_rep):
+            out.extend(r * sub + x for x in q[1:])
+        yield tuple(out)
+
+
+@dataclass
+class Plan:
+    rotation: int
+    q: tuple
+    mu: int
+    b_hat: int
+    t: list
+    u: list
+    t_rtt: float
+    cpt: float
+    memory: list = field(default_factory=list)
+
+    @property
+    def S(self) -> int:
+        return len(self.q) - 1
+
+
+class _Tables:
+    """Per-batch operator latencies, weights, KV bytes and cut handoffs of a
+    block, doubled so a rotated block is a plain slice, with prefix sums."""
+
+    def __init__(self, model: Model, g: Gpu, s: float, latency: Callable, b_hats, link_bw: float):
+        ops = block_ops(model.block)
+        self.N = len(ops)
+        self.by_b = {}
+        for b in b_hats:
+            lat = [latency(op, b, s) for op in ops] * 2
+            w = [op_bytes_flops(op.cfg, op.name, b, s)[2] for op in ops] * 2
+            kv = [op_bytes_flops(op.cfg, op.name, b, s)[3] for op in ops] * 2
+            hand = [b * handoff_bytes_per_token(op.cfg)[op.local] / link_bw for op in ops] * 2
+            pre = lambda xs: list(itertools.accumulate(xs, initial=0.0))
+            self.by_b[b] = (pre(lat), pre(w), pre(kv), hand)
+
+
+def _plan_from_tables(model: Model, g: Gpu, tab: _Tables, q: tuple, mu: int, b_hat: int, rotation: int):
+    plat, pw, pkv, hand = tab.by_b[b_hat]
+    S = len(q) - 1
+    t, u, mem = [], [], []
+    for j in range(S):
+        lo, hi = rotation + q[j], rotation + q[j + 1]
+        t.append(plat[hi] - plat[lo])
+        u.append(hand[hi - 1] if S > 1 else 0.0)
+        need = (pw[hi] - pw[lo]) * model.n_blocks + mu * b_hat * (pkv[hi] - pkv[lo]) * model.n_blocks
+        if need > g.memory:
+            return None
+        mem.append(need)
+    Bt = model.n_blocks
+    chain = Bt * sum(t) + Bt * sum(u) - (u[-1] if S > 1 else 0.0)
+    loads = [mu * Bt * tj for tj in t] + [mu * Bt * uj for uj in u[:-1]]
+    if S > 1:
+        loads.append(mu * (Bt - 1) * u[-1])
+    t_rtt = max([chain] + loads)
+    cpt = t_rtt * S * g.c / (mu * b_hat)
+    return Plan(rotation, q, mu, b_hat, t, u, t_rtt, cpt, mem)
+
+
+def evaluate(model: Model, g: Gpu, q: tuple, mu: int, b_hat: int, s: float, latency: Callable | None = None,
+             link_bw: float = 153e9, rotation: int = 0):
+    """Round-trip time, cost per token and per-owner memory of one plan on one
+    GPU type (owner m runs stage m of every block); None if a stage's memory
+    does not fit."""
+    tab = _Tables(model, g, s, latency or roofline_latency(g), (b_hat,), link_bw)
+    return _plan_from_tables(model, g, tab, q, mu, b_hat, rotation)
+
+
+def search(model: Model, g: Gpu, s: float, slo: float, latency: Callable | None = None, S_max: int = 3,
+           mus=(1, 2, 4, 8), b_hats=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), link_bw: float = 153e9,
+           rotations: bool = True):
+    """Every plan over the grid that meets the SLO and fits memory, cheapest first."""
+    tab = _Tables(model, g, s, latency or roofline_latency(g), b_hats, link_bw)
+    N = tab.N
+    out = []
+    for S in range(1, S_max + 1):
+        rots = range(N) if (rotations and S > 1) else (0,)
+        for r in rots:
+            for q in templates(N, S):
+                for mu in mus:
+                    for b in b_hats:
+                        p = _plan_from_tables(model, g, tab, q, mu, b, r)
+                        if p is not None and p.t_rtt <= slo:
+                            out.append(p)
+    out.sort(key=lambda p: p.cpt)
+    return out
+
+
+# ---------------------------------------------------------------- plans from a measured profile
+
+def named_plans(model: Model):
+    """(label, rotation, q) of the two-way templates the paper names, for a
+    one-layer dense or MoE block: AFD cuts after the output projection; CAD
+    isolates core attention (kv_append, attn_core) and lets the rest-of-model
+    stage wrap the block boundary; colocated is one stage."""
+    N = len(block_ops(model.block))
+    return [("colocated", 0, (0, N)), ("AFD", 0, (0, 6, N)), ("CAD", 5, (0, N - 2, N))]
+
+
+def profile_report(profile: dict, model: Model, g: Gpu, s: float, slo: float, S_max: int = 3,
+                   mus=(1, 2, 4, 8), b_hats=(1, 8, 32, 64, 128, 256)) -> str:
+    """Markdown table: the cheapest plan of the exhaustive search and the best
+    point of each named template, with per-operator latencies measured on the
+    GPU (profile["op_latency"])."""
+    lat = ProfiledLatency(profile["op_latency"])
+    plans = search(model, g, s, slo, lat, S_max=S_max, mus=mus, b_hats=b_hats)
+    rows = []
+    if plans:
+        p = plans[0]
+        rows.append(("search optimum", p))
+    for label, r, q in named_plans(model):
+        best = None
+        for mu in mus:
+            for b in b_hats:
+                p = _plan_from_tables(model, g, _Tables(model, g, s, lat, (b,), 153e9), q, mu, b, r)
+                if p is not None and p.t_rtt <= slo and (best is None or p.cpt < best.cpt):
+                    best = p
+        if best is not None:
+            rows.append((label, best))
+    ops = [op.name for op in block_ops(model.block)]
+    out = [f"| plan | stages (operators, block rotated by r) | mu | b_hat | T_rtt ms | stage t_j us | "
+           f"GPU-seconds per 1k tokens |", "|---|---|---:|---:|---:|---|---:|"]
+    for label, p in rows:
+        N = len(ops)
+        order = [ops[(p.rotation + i) % N] for i in range(N)]
+        stages = " / ".join(f"{order[p.q[j]]}..{order[p.q[j + 1] - 1]}" for j in range(p.S))
+        out.append(f"| {label} | r={p.rotation}: {stages} | {p.mu} | {p.b_hat} | {p.t_rtt * 1e3:.2f} | "
+                   f"{', '.join(f'{t * 1e6:.0f}' for t in p.t)} | {p.cpt / g.c * 1e3:.3f} |")
+    return "\n".join(out)
+
+
+if __name__ == "__main__":
+    import argparse
+    import json
+    import sys as _sys
+    import os as _os
+
+    _sys.path.insert(0, _os.path.dirname(_os.path.dirname(_os.path.abspath(__file__))))
+    import workloads as _W
+
+    ap = argparse.ArgumentParser(description="serving plans for the dense 8B-shaped model from a measured profile")
+    ap.add_argument("--profile", required=True, help="JSON written by bench.py --latency-table")
+    ap.add_argument("--layers", type=int, default=32)
+    ap.add_argument("--slo-ms", type=float, default=50.0)
+    args = ap.parse_args()
+    prof = json.load(open(args.profile))
+    model = Model(_W.BY_NAME["dense8b_b64"].layers, args.layers)
+    for s in (1024, 4096, 16384):
+        print(f"\n### context {s}, {args.layers} layers, TPOT SLO {args.slo_ms:g} ms, MI355X\n")
+        print(profile_report(prof, model, MI355X, s, args.slo_ms * 1e-3))

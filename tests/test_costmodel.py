@@ -1,0 +1,189 @@
+"""Cost model and planner (host side) against the paper's printed values and
+against brute force: the hardware ratios and gain bounds quoted from the GPU
+table, Theorems 1 and 2 checked numerically, b* against the operator-level
+roofline, template counts against enumeration, and plan invariants."""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import workloads as W
+from paper_2609_14237_amd import costmodel as CM
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "paper_gpu_table.txt")
+
+
+def paper_gpus():
+    gpus, pairs = {}, {}
+    for line in open(GOLDEN):
+        f = line.split()
+        if not f or f[0].startswith("#"):
+            continue
+        if "+" in f[0]:
+            pairs[f[0]] = (float(f[1]), float(f[2]))
+        else:
+            name, bw, mem, tf, price = f[0], *map(float, f[1:])
+            gpus[name] = CM.Gpu(name, price, bw * 1e9, mem * 1e9, tf * 1e12)
+    return gpus, pairs
+
+
+DENSE32 = CM.Model(W.BY_NAME["dense8b_b64"].layers, 32)
+
+
+def test_eta_and_gain_bounds_match_the_printed_examples():
+    gpus, pairs = paper_gpus()
+    for key, (eta_p, bound_p) in pairs.items():
+        a, b = key.split("+")
+        e = CM.eta(gpus[a], gpus[b])
+        assert round(e, 2) == eta_p
+        assert round(CM.g_het_bound(e), 2) == bound_p
+
+
+def test_b_star_is_where_the_operator_roofline_turns_compute_bound():
+    """b* from the closed form equals the batch at which the per-operator
+    roofline of the GEMM operators turns compute-bound when, as in Section
+    3's scaling approximations, only weight bytes count as traffic; the
+    activations each GEMM also reads and writes push the crossing higher."""
+    g = CM.MI355X
+    gemm = [op for op in CM.block_ops(DENSE32.block) if op.name in ("qkv_proj", "o_proj_residual", "gate_up",
+                                                                    "down_residual")]
+
+    def crossing(with_activations):
+        def excess(b):  # compute time minus memory time of the GEMM class at batch b
+            D = sum(CM.op_bytes_flops(op.cfg, op.name, b, 1)[0 if with_activations else 2] for op in gemm)
+            Wf = sum(CM.op_bytes_flops(op.cfg, op.name, b, 1)[1] for op in gemm)
+            return Wf / g.flops - D / g.bandwidth
+        lo, hi = 1.0, 1e5
+        for _ in range(200):
+            mid = (lo + hi) / 2
+            lo, hi = (mid, hi) if excess(mid) < 0 else (lo, mid)
+        return lo
+
+    bstar = CM.b_star(g, DENSE32)
+    assert crossing(False) == pytest.approx(bstar, rel=1e-9)
+    assert bstar < crossing(True) < 1.2 * bstar
+    assert abs(bstar - 314.6) < 0.1  # 8B-shaped layer x 32 on MI355X
+
+
+def test_theorem_1_homogeneous_gain():
+    g = CM.MI355X
+    bstar, bound = CM.b_star(g, DENSE32), CM.g_hom_bound(g, DENSE32)
+    s_max = (g.memory - DENSE32.m_weights) / DENSE32.m_kv(1)  # b_bar = 1
+    ss = np.geomspace(64, s_max * 0.999, 400)
+    gains = np.array([CM.g_hom(g, DENSE32, s) for s in ss])
+    bb = np.array([CM.b_bar(g, DENSE32, s) for s in ss])
+    assert np.all(gains[bb >= bstar] == 1.0)
+    inc = gains[bb < bstar]
+    assert np.all(inc > 1.0) and np.all(np.diff(inc) > 0)
+    assert np.all(gains < bound) and gains[-1] > 1 + 0.99 * (bound - 1)
+
+
+def test_theorem_2_heterogeneous_gain_is_unimodal_and_bounded():
+    gpus, _ = paper_gpus()
+    for a, b in (("H100", "L40S"), ("H100", "A100")):
+        g1, g2 = gpus[a], gpus[b]
+        e = CM.eta(g1, g2)
+        xs = CM.x_star(g1, g2, DENSE32)
+        # gain as a function of x = m_kv(s): m_kv is linear in s for full attention
+        per_s = DENSE32.m_kv(1.0)
+        s_star = xs / per_s
+        ss = np.geomspace(s_star / 50, s_star * 50, 801)
+        gains = np.array([CM.g_het([g1, g2], DENSE32, s) for s in ss])
+        assert np.all(gains >= 1.0) and np.all(gains <= CM.g_het_bound(e) + 1e-12)
+        k = int(np.argmax(gains))
+        assert np.all(np.diff(gains[:k + 1]) > 0) and np.all(np.diff(gains[k:]) < 0)
+        assert abs(ss[k] / s_star - 1) < 0.02
+        assert CM.g_het([g1, g2], DENSE32, s_star) >= gains.max() - 1e-12
+
+
+def test_theorem_2_bound_is_the_supremum_over_prices():
+    """Brute force over the price ratio and x reaches (1 + sqrt(eta)) / 2."""
+    gpus, _ = paper_gpus()
+    g1, g2 = gpus["H100"], gpus["A100"]
+    e = CM.eta(g1, g2)
+    best = 0.0
+    for ratio in np.geomspace(0.05, 20, 801):
+        g2r = CM.Gpu("x", g1.price_per_hour * ratio, g2.bandwidth, g2.memory, g2.flops)
+        if not (min(g1.alpha, g2r.alpha) < max(g1.alpha, g2r.alpha)):
+            continue
+        try:
+            xs = CM.x_star(g1, g2r, DENSE32)
+        except ZeroDivisionError:
+            continue
+        if xs <= 0:
+            continue
+        best = max(best, CM.g_het([g1, g2r], DENSE32, xs / DENSE32.m_kv(1.0)))
+    assert abs(best - CM.g_het_bound(e)) < 2e-3
+
+
+def test_no_heterogeneous_gain_under_dominance():
+    g1 = CM.Gpu("a", 1.0, 4e12, 80e9, 1e15)
+    g2 = CM.Gpu("b", 2.0, 3e12, 80e9, 0.9e15)  # costlier per byte and per flop
+    for s in (512, 8192, 65536):
+        assert CM.g_het([g1, g2], DENSE32, s) == pytest.approx(1.0, abs=1e-15)
+
+
+@pytest.mark.parametrize("N,S", [(10, 1), (10, 2), (10, 3), (14, 4), (9, 5)])
+def test_template_count(N, S):
+    qs = list(CM.templates(N, S))
+    assert len(qs) == len(set(qs)) == CM.count_templates(N, S) == math.comb(N - 1, S - 1)
+    assert all(q[0] == 0 and q[-1] == N and all(a < b for a, b in zip(q, q[1:])) for q in qs)
+
+
+def test_subblock_templates_tile_one_repetition():
+    N, n, K = 40, 4, 3  # the hybrid block: 4 layers of 10 operators
+    qs = list(CM.subblock_templates(N, n, K))
+    assert len(qs) == math.comb(N // n - 1, K - 1)
+    for q in qs:
+        assert len(q) - 1 == n * K
+        sub = q[:K + 1]
+        assert all(q[r * K + i] == r * (N // n) + sub[i] for r in range(n) for i in range(K + 1))
+
+
+def test_colocated_plan_is_the_roofline_step_cost():
+    """One stage, one microbatch: T_rtt is B_total times the summed operator
+    roofline latencies (Appendix A's step cost) and CPT = T_rtt c / b."""
+    g, s, b = CM.MI355X, 4096, 64
+    p = CM.evaluate(DENSE32, g, (0, 10), 1, b, s)
+    lat = CM.roofline_latency(g)
+    step = DENSE32.n_blocks * sum(lat(op, b, s) for op in CM.block_ops(DENSE32.block))
+    assert p.t_rtt == pytest.approx(step, rel=1e-12)
+    assert p.cpt == pytest.approx(step * g.c / b, rel=1e-12)
+
+
+def test_search_beats_the_named_templates_and_respects_the_slo():
+    g, s = CM.MI355X, 16384
+    block = W.BY_NAME["hybrid4_b128"].layers
+    m = CM.Model(block, 8)
+    mus, bs = (1, 2, 4), (8, 16, 32, 64, 128)
+    plans = CM.search(m, g, s, slo=0.03, S_max=2, mus=mus, b_hats=bs)
+    assert plans and all(p.t_rtt <= 0.03 for p in plans)
+    named = []
+    for q, r in (((0, 40), 0), ((0, 6, 40), 0), ((0, 38, 40), 5)):  # colocated, AFD-like, CAD-like (core attention isolated)
+        for mu in mus:
+            for b in bs:
+                p = CM.evaluate(m, g, q, mu, b, s, rotation=r)
+                if p is not None and p.t_rtt <= 0.03:
+                    named.append(p.cpt)
+    assert plans[0].cpt <= min(named) + 1e-18
+    looser = CM.search(m, g, s, slo=0.06, S_max=2, mus=mus, b_hats=bs)
+    assert looser[0].cpt <= plans[0].cpt
+
+
+def test_plans_that_do_not_fit_memory_are_dropped():
+    small = CM.Gpu("small", 1.0, 8e12, 12e9, 2.5e15)  # 12 GB: the 14 GB of weights cannot sit on one owner
+    assert CM.evaluate(DENSE32, small, (0, 10), 1, 8, 4096) is None
+    two = CM.evaluate(DENSE32, small, (0, 7, 10), 1, 8, 4096)  # attention side / FFN side each fit
+    assert two is not None and all(mem <= small.memory for mem in two.memory)
+
+
+def test_profiled_latency_interpolates_between_measured_points():
+    rows = [{"local": 0, "batch": 1, "ctx": 1024, "us": 10.0}, {"local": 0, "batch": 9, "ctx": 1024, "us": 18.0},
+            {"local": 0, "batch": 1, "ctx": 4096, "us": 20.0}, {"local": 0, "batch": 9, "ctx": 4096, "us": 36.0}]
+    lat = CM.ProfiledLatency(rows)
+    op = CM.block_ops(W.TINY.layers)[0]
+    assert lat(op, 1, 1024) == pytest.approx(10e-6)
+    assert lat(op, 5, 1024) == pytest.approx(14e-6)
+    assert lat(op, 5, 2560) == pytest.approx(21e-6)  # 14 us at 1024, 28 us at 4096
+    assert lat(op, 100, 99999) == pytest.approx(36e-6)
