@@ -17,12 +17,15 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall", "-Wno-unused-function",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", os.path.join(ROOT, "include")]
-SOURCES = ["k_gemm.hip", "k_attn.hip", "k_elem.hip", "k_moe.hip", "ods_api.cpp"]
+SOURCES = ["k_gemm.hip", "k_gemm_stream.hip", "k_attn.hip", "k_elem.hip", "k_moe.hip", "ods_api.cpp"]
+# Per-file flags: the weight-streaming GEMM keeps its MFMA accumulators in
+# VGPRs (with AGPR results the allocator copies them around the K loop).
+EXTRA = {"k_gemm_stream.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

@@ -4,9 +4,11 @@
 //
 // Tiling: 256 threads = 4 waves; block tile BM x BN outputs, K step BK; LDS
 // double buffering (global loads of step k+1 are in flight while step k runs
-// on the matrix cores). Decode GEMMs are weight-streaming (M <= 256 rows against
+// on the matrix cores). Decode GEMMs are weight-streaming (M <= 64 rows against
 // megabytes of weights), so the tile covers all rows it can and narrow outputs
-// are split along K to keep every compute unit streaming. MFMA 16x16x32 bf16: lane l holds A[m = l%16][8 k's
+// are split along K to keep every compute unit streaming. Dense GEMMs past 128
+// rows go to the direct-to-LDS streaming kernel (k_gemm_stream.hip); the
+// large-M kernel here takes 64 < M <= 128 and the grouped expert GEMMs. MFMA 16x16x32 bf16: lane l holds A[m = l%16][8 k's
 // starting at (l/16)*8] and B[same k's][n = l%16]; the 16x16 fp32 result puts
 // rows (l/16)*4 .. +3 of column l%16 in lane l.
 #include "common.hpp"
@@ -173,8 +175,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs p) {
   }
 }
 
-// Large-M variant (M > 64: the 256-row decode batch, the 512-row MoE
-// attention projections): 512 threads = 8 waves as 4 (M) x 2 (N), block tile
+// Large-M variant (grouped expert GEMMs; dense GEMMs with 64 < M <= 128 or K
+// not a multiple of 64): 512 threads = 8 waves as 4 (M) x 2 (N), block tile
 // BM x BN with BN = 128 columns of B rows (SiLU: 64 gate + 64 up rows), wave
 // tile (BM/4) x 64. The whole batch fits one or two M tiles, so the weights
 // stream from HBM once. Pipeline: step k+1 arrives in registers while step k
@@ -453,6 +455,7 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
   }
   const bool part = a.splits > 1;
   hipError_t e;
+  if (gemm_use_stream(a.M, a.N, a.K)) return launch_gemm_stream(a, s);  // launches its own reduce
   if (use_big(a.M, a.N)) {
     const int bm = a.M > 128 ? 256 : 128;
     const int bnb = EPI == EPI_SILU ? 64 : 128;
@@ -470,14 +473,13 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
     e = part ? launch_tile<kBM, 64, kBK, EPI, true>(a, grid, s) : launch_tile<kBM, 64, kBK, EPI, false>(a, grid, s);
   }
   if (e != hipSuccess || !part) return e;
-  const int64_t quads = (int64_t)a.M * a.N / 4;
-  hipLaunchKernelGGL((splitk_reduce_kernel<EPI>), dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, s, a);
-  return hipGetLastError();
+  return launch_splitk_reduce(a, s);
 }
 
 }  // namespace
 
 int gemm_splits(int M, int N, int K, int epi) {
+  if (gemm_use_stream(M, N, K)) return gemm_stream_splits(M, N, K, epi);
   if (N % 4 != 0) return 1;  // the reduce works on 4-column groups
   if (use_big(M, N)) {
     // Large-M tiles: one 512-thread block per compute unit; split K (up to 8
@@ -509,6 +511,18 @@ size_t gemm_partial_bytes(int M, int N, int K, int epi) {
   const int s = gemm_splits(M, N, K, epi);
   if (s <= 1) return 0;
   return (size_t)s * M * N * (epi == EPI_SILU ? 2 : 1) * sizeof(float);
+}
+
+hipError_t launch_splitk_reduce(const GemmArgs &a, hipStream_t s) {
+  const int64_t quads = (int64_t)a.M * a.N / 4;
+  const dim3 grid((unsigned)((quads + 255) / 256));
+  switch (a.epi) {
+    case EPI_BF16: hipLaunchKernelGGL((splitk_reduce_kernel<EPI_BF16>), grid, dim3(256), 0, s, a); break;
+    case EPI_F32: hipLaunchKernelGGL((splitk_reduce_kernel<EPI_F32>), grid, dim3(256), 0, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((splitk_reduce_kernel<EPI_RESID>), grid, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((splitk_reduce_kernel<EPI_SILU>), grid, dim3(256), 0, s, a); break;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {

@@ -33,6 +33,12 @@ int num_cus();
 int gemm_splits(int M, int N, int K, int epi);
 size_t gemm_partial_bytes(int M, int N, int K, int epi);
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
+// Sum of split-K partials plus the epilogue (after a partial-writing launch).
+hipError_t launch_splitk_reduce(const GemmArgs &a, hipStream_t s);
+// Weight-streaming kernel for dense GEMMs past 128 rows (K % 64 == 0).
+bool gemm_use_stream(int M, int N, int K);
+int gemm_stream_splits(int M, int N, int K, int epi);
+hipError_t launch_gemm_stream(const GemmArgs &a, hipStream_t s);
 
 hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gain, uint16_t *out, int rows, int H,
                           float eps, hipStream_t s);
