@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--workload", default="dense8b_b64")
     ap.add_argument("--copies", type=int, default=0, help="weight/KV copies in rotation (0: auto)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--swa-ring", action="store_true",
+                    help="sliding-window layers keep their KV in a window-only page ring "
+                         "(ceil(window / 16) + 1 pages per sequence) instead of full page tables")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work to time")
     ap.add_argument("--ffn-sweep", action="store_true",
                     help="instead of the decode step, time the dense FFN stage alone over batch sizes "
@@ -323,15 +326,28 @@ def main():
     step_bytes = sum(a["attn_bytes"] + a["ffn_bytes"] for a in acct)
     copies = args.copies or (3 if step_bytes < 2e9 else 1)
 
-    batch = R.DeviceBatch(torch.from_numpy(ctx).to(dev), torch.from_numpy(page_table).to(dev))
+    # window-only page ring for the sliding-window layers (same attended bytes, bounded memory)
+    ring_pages, ring_table, P_ring = 0, None, 0
+    windows = [c.window for c in w.layers if c.window > 0]
+    if args.swa_ring and windows:
+        ring_pages = max(-(-win // 16) + 1 for win in windows)
+        rctx = np.minimum(ctx, 16 * ring_pages).astype(np.int32)
+        P_ring = gen.pool_pages_for(rctx)
+        ring_table = np.zeros((w.batch, ring_pages), dtype=np.int32)
+        assert B.ods_kv_alloc(P_ring, rctx, w.batch, w.seed + 7, ring_pages, ring_table) == 0, B.ods_last_error()
+    layer_pages = [P_ring if (ring_pages and c.window > 0) else P for c in w.layers]
+    kv_pool_bytes = [B.ods_kv_pool_bytes(R.layer_cfg(c), n) for c, n in zip(w.layers, layer_pages)]
+
+    batch = R.DeviceBatch(torch.from_numpy(ctx).to(dev), torch.from_numpy(page_table).to(dev),
+                          ring_table=None if ring_table is None else torch.from_numpy(ring_table).to(dev))
     sets = []
     for c in range(copies):
         seed = w.seed + 1000 * c
         weights = [{k: v for k, v in gen.layer_weights(cfg, seed, l, dev, w.router_std).items()}
                    for l, cfg in enumerate(w.layers)]
-        pools = [gen.kv_pool(cfg, P, seed, l, dev) for l, cfg in enumerate(w.layers)]
+        pools = [gen.kv_pool(cfg, n, seed, l, dev) for l, (cfg, n) in enumerate(zip(w.layers, layer_pages))]
         x = gen.activations(w.batch, w.layers[0].hidden, seed, dev)
-        blk = R.DeviceBlock(w.layers, weights, pools, P)
+        blk = R.DeviceBlock(w.layers, weights, pools, layer_pages)
         state = R.DeviceState(blk, batch, dev)
         sets.append(dict(block=blk, state=state, weights=weights, pools=pools, x=x, ctx=ctx,
                          page_table=page_table))
@@ -440,7 +456,9 @@ def main():
         "config": {"workload": w.name, "description": w.description, "batch": w.batch,
                    "ctx_range": [w.ctx_lo, w.ctx_hi], "ctx_mean": float(ctx.mean()),
                    "layers": n_layers, "copies_rotated": copies,
-                   "step": "attention stage [0,6) then FFN stage [6,N) per layer"},
+                   "step": "attention stage [0,6) then FFN stage [6,N) per layer",
+                   "kv_ring_pages": ring_pages, "kv_pool_bytes_per_layer": kv_pool_bytes,
+                   "kv_pool_bytes_total": int(sum(kv_pool_bytes))},
         "stages": {"attn": stage(t_attn, attn_bytes, attn_flops), "ffn": stage(t_ffn, ffn_bytes, ffn_flops)},
         "handoff": {"cut": "after local op 5 (attention stage | FFN stage)",
                     "bytes_per_token": handoff_bytes_per_token(w.layers[0])["5"],
@@ -451,7 +469,7 @@ def main():
                      "traffic": traffic,
                      "algorithmic_bytes_per_launch": core_bytes, "avg_launch_us": t_core * 1e6},
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not ring_pages:  # the oracle baseline reads the full page tables
         result["cpu_baseline"] = cpu_baseline(w, sets[0], args.cpu_budget)
     print(json.dumps(result), flush=True)
 

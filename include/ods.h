@@ -125,12 +125,28 @@ typedef struct {
  * equal contiguous range of them; split_pages fixes the range length in pages
  * (0: library choice, the batch's pages over all waves, at least 8 each).
  * attn_core takes batch <= 4096 and batch * n_kv * window pages < 2^30
- * (ODS_EUNSUPPORTED otherwise). */
+ * (ODS_EUNSUPPORTED otherwise).
+ *
+ * Window-only page ring (ring_pages > 0). A sliding-window layer only ever
+ * reads the most recent `window` tokens, so its KV pages can live in a ring
+ * (the paper's hybrid-architecture discussion: efficient attention operators
+ * access a bounded window, Section 3): with ring_pages = R > 0, every layer of
+ * the call with window > 0 maps token position t of sequence b to page
+ * ring_table[b][(t / 16) % R], slot t % 16, of its own kv_pool, and its
+ * contexts are not clamped to max_pages * 16. Full-attention layers keep
+ * page_table. R must be at least ceil(window / 16) + 1 for every such layer
+ * the call touches (the window's pages plus the one the next token opens), so
+ * a page is only reused once it has left the window (ODS_EINVAL otherwise).
+ * ring_table is [batch][R] int32; ods_kv_alloc with max_pages = R and contexts
+ * min(ctx, 16 R) fills one. A ring layer's pool needs at most batch * R pages
+ * however long the contexts grow. ring_pages = 0: no ring (ring_table unused). */
 typedef struct {
   int32_t batch, max_pages;
   const int32_t *ctx_lens;
   const int32_t *page_table;
   int32_t split_pages;
+  int32_t ring_pages;
+  const int32_t *ring_table;
 } ods_batch;
 
 /* Live buffers (the activation interface at any cut), device, caller-allocated.

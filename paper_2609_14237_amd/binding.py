@@ -40,7 +40,8 @@ class ods_block(C.Structure):
 
 class ods_batch(C.Structure):
     _fields_ = [("batch", C.c_int32), ("max_pages", C.c_int32), ("ctx_lens", C.c_void_p),
-                ("page_table", C.c_void_p), ("split_pages", C.c_int32)]
+                ("page_table", C.c_void_p), ("split_pages", C.c_int32), ("ring_pages", C.c_int32),
+                ("ring_table", C.c_void_p)]
 
 
 class ods_state(C.Structure):

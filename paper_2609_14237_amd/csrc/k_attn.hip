@@ -65,7 +65,7 @@ __device__ __forceinline__ void window_of(int ctx, int window, int &p, int &lo, 
 template <int D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) void attn_flat_kernel(
     const uint16_t *__restrict__ qkv, int n_q, int n_kv, int window, const int32_t *__restrict__ ctx_lens,
-    const int32_t *__restrict__ page_table, int max_pages, const uint16_t *__restrict__ pool,
+    const int32_t *__restrict__ page_table, int max_pages, int ring, const uint16_t *__restrict__ pool,
     int64_t pool_pages, int seg_pages, float scale_log2, float *__restrict__ ws_acc, float *__restrict__ ws_ml,
     int2 *__restrict__ ws_meta, uint16_t *__restrict__ o, int B) {
   constexpr int KK = D / 32;  // QK MFMAs per page
@@ -73,7 +73,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) voi
   constexpr int64_t BLK = (int64_t)kPage * D;
   extern __shared__ int smem_i[];
   int *s_pre = smem_i;          // [B + 1]: first unit of sequence b (its KV head 0)
-  int *s_ctx = smem_i + B + 1;  // [B]: context clamped to the page table
+  int *s_ctx = smem_i + B + 1;  // [B]: context (clamped to the page table unless it is a ring)
   __shared__ int s_wtot[4];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -90,7 +90,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) voi
     const int b0 = min(B, tid * per), b1 = min(B, b0 + per);
     int loc = 0;
     for (int b = b0; b < b1; ++b) {
-      const int c = min(ctx_lens[b], max_pages * kPage);
+      const int c = ring > 0 ? ctx_lens[b] : min(ctx_lens[b], max_pages * kPage);
       int p, lo, fp, n;
       window_of(c, window, p, lo, fp, n);
       s_ctx[b] = c;
@@ -142,8 +142,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) voi
       const int b = find_seq(u);
       int p, lo, fp, n;
       window_of(s_ctx[b], window, p, lo, fp, n);
-      const int page = (u - s_pre[b]) % n;
-      return page_table[(int64_t)b * max_pages + fp + page];
+      const int lp = fp + (u - s_pre[b]) % n;  // logical page of the sequence
+      return page_table[(int64_t)b * max_pages + (ring > 0 ? lp % ring : lp)];
     };
 
     // ---- issue cursor: the next range page to load, as (sequence, head, window page)
@@ -424,7 +424,7 @@ size_t attn_ws_bytes(int B, int n_q, int n_kv, int D, const AttnPlan &plan) {
 }
 
 hipError_t launch_attention(const uint16_t *qkv, int B, int n_q, int n_kv, int D, int window,
-                            const int32_t *ctx_lens, const int32_t *page_table, int max_pages,
+                            const int32_t *ctx_lens, const int32_t *page_table, int max_pages, int ring,
                             const uint16_t *pool, int64_t pool_pages, const AttnPlan &plan, float *ws,
                             uint16_t *o, hipStream_t s) {
   if (B <= 0) return hipSuccess;
@@ -437,7 +437,7 @@ hipError_t launch_attention(const uint16_t *qkv, int B, int n_q, int n_kv, int D
   const dim3 mgrid((unsigned)(((int64_t)B * n_q + 3) / 4));
   auto go = [&](auto kflat, auto kmerge) {
     hipLaunchKernelGGL(kflat, dim3(plan.grid), dim3(256), lds, s, qkv, n_q, n_kv, window, ctx_lens, page_table,
-                       max_pages, pool, pool_pages, plan.seg_pages, scale_log2, ws_acc, ws_ml, ws_meta, o, B);
+                       max_pages, ring, pool, pool_pages, plan.seg_pages, scale_log2, ws_acc, ws_ml, ws_meta, o, B);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kmerge, mgrid, dim3(256), 0, s, ws_acc, ws_ml, ws_meta, n_q, n_kv, ctx_lens, o, B);

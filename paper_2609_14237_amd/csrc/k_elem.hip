@@ -40,19 +40,20 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t *x, const u
 
 // One block per sequence. RoPE (rotate-half) of the n_q + n_kv heads of
 // qkv[b] at position ctx[b] - 1, in place, and/or store of k, v into the page
-// slot of that position. The angle p * theta^(-2i/d) is formed in double and
+// slot of that position. With ring > 0 the table is a window-only page ring:
+// position p lives in page_table[b][(p / 16) % ring] and is not clamped. The angle p * theta^(-2i/d) is formed in double and
 // reduced modulo 2 pi there, so the fp32 sin / cos see |r| <= pi (positions
 // reach 10^5 radians, where an fp32 angle would keep only ~2 decimals).
 __global__ __launch_bounds__(256) void rope_append_kernel(uint16_t *qkv, int n_q, int n_kv, int D,
                                                           float theta, const int32_t *ctx_lens,
-                                                          const int32_t *page_table, int max_pages,
+                                                          const int32_t *page_table, int max_pages, int ring,
                                                           uint16_t *pool, int64_t pool_pages,
                                                           int do_rope, int do_append) {
   __shared__ float cs[64], sn[64];
   const int b = blockIdx.x;
   const int ctx = ctx_lens[b];
   if (ctx < 1) return;
-  const int p = min(ctx, max_pages * kPage) - 1;
+  const int p = (ring > 0 ? ctx : min(ctx, max_pages * kPage)) - 1;
   const int half = D / 2, nvh = half / 8;
   uint16_t *row = qkv + (int64_t)b * (n_q + 2 * n_kv) * D;
 
@@ -60,7 +61,7 @@ __global__ __launch_bounds__(256) void rope_append_kernel(uint16_t *qkv, int n_q
   const int64_t blk = (int64_t)kPage * D;
   const int slot = p % kPage;
   if (do_append) {
-    const int page = page_table[(int64_t)b * max_pages + p / kPage];
+    const int page = page_table[(int64_t)b * max_pages + (ring > 0 ? (p / kPage) % ring : p / kPage)];
     if (page >= 0 && page < pool_pages) {
       kbase = pool + (int64_t)page * 2 * n_kv * blk;
       vbase = kbase + n_kv * blk;
@@ -140,12 +141,12 @@ hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gain, uint16_t *out
 }
 
 hipError_t launch_rope_append(uint16_t *qkv, int B, int n_q, int n_kv, int D, float theta,
-                              const int32_t *ctx_lens, const int32_t *page_table, int max_pages,
+                              const int32_t *ctx_lens, const int32_t *page_table, int max_pages, int ring,
                               uint16_t *pool, int64_t pool_pages, bool do_rope, bool do_append,
                               hipStream_t s) {
   if (B <= 0) return hipSuccess;
   hipLaunchKernelGGL(rope_append_kernel, dim3(B), dim3(256), 0, s, qkv, n_q, n_kv, D, theta, ctx_lens,
-                     page_table, max_pages, pool, pool_pages, (int)do_rope, (int)do_append);
+                     page_table, max_pages, ring, pool, pool_pages, (int)do_rope, (int)do_append);
   return hipGetLastError();
 }
 

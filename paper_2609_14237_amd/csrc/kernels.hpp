@@ -44,8 +44,10 @@ hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gain, uint16_t *out
                           float eps, hipStream_t s);
 
 // In-place RoPE of the q and k heads of qkv and/or append of k, v to the KV pool.
+// ring > 0: page_table is a [B][ring] window-only page ring (logical page lp in
+// column lp % ring, contexts not clamped); max_pages is then ring.
 hipError_t launch_rope_append(uint16_t *qkv, int B, int n_q, int n_kv, int D, float theta,
-                              const int32_t *ctx_lens, const int32_t *page_table, int max_pages,
+                              const int32_t *ctx_lens, const int32_t *page_table, int max_pages, int ring,
                               uint16_t *pool, int64_t pool_pages, bool do_rope, bool do_append,
                               hipStream_t s);
 
@@ -61,7 +63,7 @@ struct AttnPlan {
 AttnPlan attn_plan(int B, int n_kv, int D, int max_pages, int window, int split_pages_req);
 size_t attn_ws_bytes(int B, int n_q, int n_kv, int D, const AttnPlan &plan);
 hipError_t launch_attention(const uint16_t *qkv, int B, int n_q, int n_kv, int D, int window,
-                            const int32_t *ctx_lens, const int32_t *page_table, int max_pages,
+                            const int32_t *ctx_lens, const int32_t *page_table, int max_pages, int ring,
                             const uint16_t *pool, int64_t pool_pages, const AttnPlan &plan,
                             float *ws, uint16_t *o, hipStream_t s);
 

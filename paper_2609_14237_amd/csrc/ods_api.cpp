@@ -107,8 +107,21 @@ int layer_offset(const ods_block *blk, int layer) {
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Page table a layer's KV operators use: the window-only ring for a sliding-
+// window layer when the batch carries one, the full page table otherwise.
+struct KvMap {
+  const int32_t *table;
+  int cols;  // table columns
+  int ring;  // > 0: logical page lp lives in column lp % ring
+};
+
+KvMap kv_map(const ods_layer_cfg &c, const ods_batch *b) {
+  if (c.window > 0 && b->ring_pages > 0) return KvMap{b->ring_table, b->ring_pages, b->ring_pages};
+  return KvMap{b->page_table, b->max_pages, 0};
+}
+
 AttnPlan plan_for(const ods_layer_cfg &c, const ods_batch *b) {
-  return attn_plan(b->batch, c.n_kv, c.head_dim, b->max_pages, c.window, b->split_pages);
+  return attn_plan(b->batch, c.n_kv, c.head_dim, kv_map(c, b).cols, c.window, b->split_pages);
 }
 
 size_t layer_ws_bytes(const ods_layer_cfg &c, const ods_batch *b) {
@@ -242,6 +255,7 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
   const int B = batch->batch;
   if (B < 0) return fail(ODS_EINVAL, "negative batch");
   if (batch->split_pages < 0) return fail(ODS_EINVAL, "negative split_pages");
+  if (batch->ring_pages < 0) return fail(ODS_EINVAL, "negative ring_pages");
 
   // ---- validation pass: every pointer an operator in the range touches ----
   std::vector<OpRef> ops;
@@ -261,7 +275,8 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
       case K_ROPE: need = {{st->qkv, "qkv"}, {batch->ctx_lens, "ctx_lens"}}; paged = true; break;
       case K_KV_APPEND:
       case K_ATTN_CORE:
-        need = {{st->qkv, "qkv"}, {batch->ctx_lens, "ctx_lens"}, {batch->page_table, "page_table"},
+        need = {{st->qkv, "qkv"}, {batch->ctx_lens, "ctx_lens"},
+                {kv_map(c, batch).table, kv_map(c, batch).ring ? "ring_table" : "page_table"},
                 {L.kv_pool, "kv_pool"}};
         if (k == K_ATTN_CORE) {
           need.push_back({st->o, "o"});
@@ -311,6 +326,13 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
       if (batch->max_pages <= 0) return fail(ODS_EINVAL, "max_pages must be positive");
       if ((int64_t)batch->max_pages * ODS_PAGE_TOKENS > INT32_MAX) return fail(ODS_ERANGE, "max_pages too large");
       if (k != K_ROPE && L.pool_pages <= 0) return fail(ODS_EINVAL, "layer %d: pool_pages <= 0", ops[i].layer);
+      const KvMap m = kv_map(c, batch);
+      if (m.ring > 0) {
+        const int64_t need_pages = ((int64_t)c.window + ODS_PAGE_TOKENS - 1) / ODS_PAGE_TOKENS + 1;
+        if (m.ring < need_pages)
+          return fail(ODS_EINVAL, "layer %d: ring_pages %d < ceil(window / 16) + 1 = %lld", ops[i].layer, m.ring,
+                      (long long)need_pages);
+      }
     }
     if (is_moe(c) && (int64_t)B * c.top_k > INT32_MAX / 2) return fail(ODS_ERANGE, "batch * top_k too large");
   }
@@ -360,9 +382,9 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
       case K_ROPE:
       case K_KV_APPEND: {
         const bool both = k == K_ROPE && next_same_layer && ops[i + 1].kind == K_KV_APPEND;
-        e = launch_rope_append(U(st->qkv), B, c.n_q, c.n_kv, D, c.rope_theta, batch->ctx_lens, batch->page_table,
-                               batch->max_pages, U(L.kv_pool), L.pool_pages, k == K_ROPE, both || k == K_KV_APPEND,
-                               stream);
+        const KvMap m = kv_map(c, batch);
+        e = launch_rope_append(U(st->qkv), B, c.n_q, c.n_kv, D, c.rope_theta, batch->ctx_lens, m.table, m.cols,
+                               m.ring, U(L.kv_pool), L.pool_pages, k == K_ROPE, both || k == K_KV_APPEND, stream);
         if (both) {
           what = "rope+kv_append";
           ++i;
@@ -370,10 +392,12 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
         break;
       }
       case K_ATTN_CORE:
-        e = launch_attention(U(st->qkv), B, c.n_q, c.n_kv, D, c.window, batch->ctx_lens, batch->page_table,
-                             batch->max_pages, U(L.kv_pool), L.pool_pages, plan_for(c, batch), (float *)st->ws,
-                             U(st->o), stream);
+      {
+        const KvMap m = kv_map(c, batch);
+        e = launch_attention(U(st->qkv), B, c.n_q, c.n_kv, D, c.window, batch->ctx_lens, m.table, m.cols, m.ring,
+                             U(L.kv_pool), L.pool_pages, plan_for(c, batch), (float *)st->ws, U(st->o), stream);
         break;
+      }
       case K_O_PROJ: e = dense_gemm(st->o, L.w_o, st->resid, H, c.n_q * D, EPI_RESID, 0, H); break;
       case K_GATE_UP:
         if (next_same_layer && ops[i + 1].kind == K_SILU) {

@@ -24,13 +24,15 @@ def _ptr(t):
 
 
 class DeviceBlock:
-    """ods_block over per-layer weight dicts and KV pools (tensors stay referenced)."""
+    """ods_block over per-layer weight dicts and KV pools (tensors stay referenced).
+    pool_pages is one count for every layer or a list with one per layer."""
 
-    def __init__(self, cfgs, weights, pools, pool_pages: int):
+    def __init__(self, cfgs, weights, pools, pool_pages):
         self.cfgs = list(cfgs)
         self.weights = list(weights)
         self.pools = list(pools)
         n = len(self.cfgs)
+        pages = list(pool_pages) if isinstance(pool_pages, (list, tuple)) else [pool_pages] * n
         self._layers = (ods_layer * n)()
         for i, (cfg, w, pool) in enumerate(zip(self.cfgs, self.weights, self.pools)):
             L = self._layers[i]
@@ -38,7 +40,7 @@ class DeviceBlock:
             for name in ("g_attn", "w_qkv", "w_o", "g_ffn", "w_gate_up", "w_down", "w_router"):
                 setattr(L, name, _ptr(w.get(name)))
             L.kv_pool = _ptr(pool)
-            L.pool_pages = pool_pages if pool is not None else 0
+            L.pool_pages = pages[i] if pool is not None else 0
         self.c = ods_block(n, C.cast(self._layers, C.POINTER(ods_layer)))
 
     def num_ops(self) -> int:
@@ -52,14 +54,22 @@ class DeviceBlock:
 
 
 class DeviceBatch:
-    """ods_batch over device int32 ctx_lens [B] and page_table [B, max_pages]."""
+    """ods_batch over device int32 ctx_lens [B] and page_table [B, max_pages], and
+    optionally a window-only page ring [B, ring_pages] for sliding-window layers."""
 
-    def __init__(self, ctx_lens: torch.Tensor, page_table: torch.Tensor, split_pages: int = 0):
+    def __init__(self, ctx_lens: torch.Tensor, page_table: torch.Tensor, split_pages: int = 0,
+                 ring_table: torch.Tensor | None = None):
         assert ctx_lens.dtype == torch.int32 and page_table.dtype == torch.int32
         self.ctx_lens = ctx_lens.contiguous()
         self.page_table = page_table.contiguous()
+        self.ring_table = None if ring_table is None else ring_table.contiguous()
         B, max_pages = self.page_table.shape
-        self.c = ods_batch(B, max_pages, _ptr(self.ctx_lens), _ptr(self.page_table), split_pages)
+        ring_pages = 0
+        if self.ring_table is not None:
+            assert self.ring_table.dtype == torch.int32 and self.ring_table.shape[0] == B
+            ring_pages = self.ring_table.shape[1]
+        self.c = ods_batch(B, max_pages, _ptr(self.ctx_lens), _ptr(self.page_table), split_pages, ring_pages,
+                           _ptr(self.ring_table))
 
     @property
     def batch(self) -> int:

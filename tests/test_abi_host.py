@@ -170,3 +170,22 @@ def test_graph_entry_points_reject_null_handles():
     assert B.lib.ods_partition_graph(C.byref(blk.c), 0, 1, C.byref(batch), C.byref(state), None) == B.ODS_EINVAL
     assert B.ods_graph_launch(None, 0) == B.ODS_EINVAL
     assert B.ods_graph_destroy(None) == B.ODS_OK
+
+
+def test_ring_pages_validation():
+    """A window-only ring must hold the window's pages plus the next one."""
+    from dataclasses import replace as _r
+    cfg = _r(W.TINY.layers[0], window=64)  # needs ceil(64 / 16) + 1 = 5 ring pages
+    blk = fake_block([cfg])
+    for ring in (4, -1):
+        batch = B.ods_batch(4, 8, FAKE, FAKE, 0, ring, FAKE)
+        assert B.ods_run_partition(blk.c, 4, 5, batch, fake_state(), 0) == B.ODS_EINVAL, ring
+        assert "ring" in B.ods_last_error()
+    # a ring with a null table is rejected by name for the KV operators of a window layer
+    batch = B.ods_batch(4, 8, FAKE, FAKE, 0, 5, None)
+    assert B.ods_run_partition(blk.c, 3, 4, batch, fake_state(), 0) == B.ODS_EINVAL
+    assert "ring_table" in B.ods_last_error()
+    # full-attention layers ignore the ring (no validation against it)
+    full = fake_block([W.TINY.layers[0]])
+    batch = B.ods_batch(4, 8, FAKE, FAKE, 0, 1, None)
+    assert B.ods_workspace_bytes(full.c, batch) > 0
