@@ -38,24 +38,42 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t *x, const u
   }
 }
 
-// One block per sequence. RoPE (rotate-half) of the n_q + n_kv heads of
-// qkv[b] at position ctx[b] - 1, in place, and/or store of k, v into the page
-// slot of that position. With ring > 0 the table is a window-only page ring:
-// position p lives in page_table[b][(p / 16) % ring] and is not clamped. The angle p * theta^(-2i/d) is formed in double and
-// reduced modulo 2 pi there, so the fp32 sin / cos see |r| <= pi (positions
-// reach 10^5 radians, where an fp32 angle would keep only ~2 decimals).
+// One block per (sequence, group of kRopeHeads heads of its qkv row). RoPE
+// (rotate-half) of the group's q and k heads at position ctx[b] - 1, in place,
+// and/or store of its k, v heads into the page slot of that position. With
+// ring > 0 the table is a window-only page ring: position p lives in
+// page_table[b][(p / 16) % ring] and is not clamped. With splits > 1 the
+// group's columns of the row are first summed from the split-K partials.
+constexpr int kRopeHeads = 8;
+
 __global__ __launch_bounds__(256) void rope_append_kernel(uint16_t *qkv, int n_q, int n_kv, int D,
                                                           float theta, const int32_t *ctx_lens,
                                                           const int32_t *page_table, int max_pages, int ring,
                                                           uint16_t *pool, int64_t pool_pages,
-                                                          int do_rope, int do_append) {
+                                                          int do_rope, int do_append, const float *partial,
+                                                          int splits, int B) {
   __shared__ float cs[64], sn[64];
   const int b = blockIdx.x;
+  const int nh = n_q + 2 * n_kv, W = nh * D;
+  const int h0 = blockIdx.y * kRopeHeads, h1 = min(nh, h0 + kRopeHeads);
+  uint16_t *row = qkv + (int64_t)b * W;
+  if (splits > 1) {
+    // columns of heads [h0, h1) = bf16(sum over s of partial[s][b]), 4 per
+    // thread, splits in order: what the split-K reduce would have written.
+    for (int c = h0 * D + threadIdx.x * 4; c < h1 * D; c += 256 * 4) {
+      f32x4 v = {0.f, 0.f, 0.f, 0.f};
+      for (int sp = 0; sp < splits; ++sp) v += *(const f32x4 *)(partial + ((int64_t)sp * B + b) * W + c);
+      u32x2 o;
+      o[0] = pack2(v[0], v[1]);
+      o[1] = pack2(v[2], v[3]);
+      *(u32x2 *)(row + c) = o;
+    }
+    __syncthreads();  // the columns are read back below by other threads of this block
+  }
   const int ctx = ctx_lens[b];
   if (ctx < 1) return;
   const int p = (ring > 0 ? ctx : min(ctx, max_pages * kPage)) - 1;
   const int half = D / 2, nvh = half / 8;
-  uint16_t *row = qkv + (int64_t)b * (n_q + 2 * n_kv) * D;
 
   uint16_t *kbase = nullptr, *vbase = nullptr;
   const int64_t blk = (int64_t)kPage * D;
@@ -67,7 +85,9 @@ __global__ __launch_bounds__(256) void rope_append_kernel(uint16_t *qkv, int n_q
       vbase = kbase + n_kv * blk;
     }
   }
-  if (do_rope) {
+  // q and k heads of the group: rotate (if asked) 8 pairs per item; k heads also go to the cache
+  const int qk0 = max(h0, do_rope ? 0 : n_q), qk1 = min(h1, n_q + n_kv);
+  if (do_rope && qk0 < qk1) {
     if (threadIdx.x < half) {
       const double two_pi_hi = 6.283185307179586, two_pi_lo = 2.4492935982947064e-16;
       const double inv = exp2(-(2.0 * threadIdx.x / D) * log2((double)theta));
@@ -81,11 +101,9 @@ __global__ __launch_bounds__(256) void rope_append_kernel(uint16_t *qkv, int n_q
     }
     __syncthreads();
   }
-  // q and k heads: rotate (if asked) 8 pairs per item; k heads also go to the cache
-  const int first = do_rope ? 0 : n_q;
-  const int items = (n_q + n_kv - first) * nvh;
+  const int items = max(0, qk1 - qk0) * nvh;
   for (int t = threadIdx.x; t < items; t += 256) {
-    const int h = first + t / nvh, i0 = (t % nvh) * 8;
+    const int h = qk0 + t / nvh, i0 = (t % nvh) * 8;
     uint16_t *u = row + h * D;
     u32x4 x0 = *(const u32x4 *)(u + i0), x1 = *(const u32x4 *)(u + half + i0);
     if (do_rope) {
@@ -108,12 +126,12 @@ __global__ __launch_bounds__(256) void rope_append_kernel(uint16_t *qkv, int n_q
       *(u32x4 *)(dst + half + i0) = x1;
     }
   }
-  // v heads: dim-major in the page, one element per store
-  if (vbase) {
-    const uint16_t *v = row + (n_q + n_kv) * D;
-    for (int t = threadIdx.x; t < n_kv * D; t += 256) {
-      const int g = t / D, i = t % D;
-      vbase[g * blk + i * kPage + slot] = v[t];
+  // v heads of the group: dim-major in the page, one element per store
+  const int v0 = max(h0, n_q + n_kv);
+  if (vbase && v0 < h1) {
+    for (int t = threadIdx.x; t < (h1 - v0) * D; t += 256) {
+      const int g = v0 - (n_q + n_kv) + t / D, i = t % D;
+      vbase[g * blk + i * kPage + slot] = row[(int64_t)(v0 - (n_q + n_kv)) * D + (n_q + n_kv) * D + t];
     }
   }
 }
@@ -143,10 +161,12 @@ hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gain, uint16_t *out
 hipError_t launch_rope_append(uint16_t *qkv, int B, int n_q, int n_kv, int D, float theta,
                               const int32_t *ctx_lens, const int32_t *page_table, int max_pages, int ring,
                               uint16_t *pool, int64_t pool_pages, bool do_rope, bool do_append,
-                              hipStream_t s) {
+                              hipStream_t s, const float *partial, int splits) {
   if (B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(rope_append_kernel, dim3(B), dim3(256), 0, s, qkv, n_q, n_kv, D, theta, ctx_lens,
-                     page_table, max_pages, ring, pool, pool_pages, (int)do_rope, (int)do_append);
+  const int groups = (n_q + 2 * n_kv + kRopeHeads - 1) / kRopeHeads;
+  hipLaunchKernelGGL(rope_append_kernel, dim3(B, groups), dim3(256), 0, s, qkv, n_q, n_kv, D, theta, ctx_lens,
+                     page_table, max_pages, ring, pool, pool_pages, (int)do_rope, (int)do_append, partial,
+                     partial ? splits : 1, B);
   return hipGetLastError();
 }
 

@@ -438,11 +438,19 @@ bool use_big(int M, int N) { return M > kBM && N > 128; }
 
 // Output tile width: 32 columns for narrow outputs (more blocks), 64 otherwise.
 // SiLU-gated outputs count gate and up rows, so their tile is half as wide.
-int tile_n(int N, int epi) { return (epi == EPI_SILU ? 2 * N : N) <= 8192 ? 32 : (epi == EPI_SILU ? 32 : 64); }
+// A long-K narrow output (K >= 2N, the down projection) takes 64 columns: every
+// block re-reads the activation rows of its K range, and at 32 columns those
+// re-reads cost twice the weight bytes (down at M = 64: 38.4 -> 31.3 us with
+// 8-way split-K restoring the block count).
+bool long_k(int N, int K, int epi) { return epi != EPI_SILU && N > 128 && K >= 2 * N; }
+int tile_n(int N, int K, int epi) {
+  if (long_k(N, K, epi)) return 64;
+  return (epi == EPI_SILU ? 2 * N : N) <= 8192 ? 32 : (epi == EPI_SILU ? 32 : 64);
+}
 
 template <int EPI>
 hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
-  const int bn = tile_n(a.N, EPI);
+  const int bn = tile_n(a.N, a.K, EPI);
   const int n_tiles = (a.N + bn - 1) / bn;
   if (a.group_off) {
     // Expert row groups average B*k/E rows (64 at the MoE workload): a
@@ -472,7 +480,7 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
   else
     e = part ? launch_tile<kBM, 64, kBK, EPI, true>(a, grid, s) : launch_tile<kBM, 64, kBK, EPI, false>(a, grid, s);
   }
-  if (e != hipSuccess || !part) return e;
+  if (e != hipSuccess || !part || a.defer_reduce) return e;
   return launch_splitk_reduce(a, s);
 }
 
@@ -491,18 +499,18 @@ int gemm_splits(int M, int N, int K, int epi) {
     while (tiles * s < 192 && s < 8 && steps / (s * 2) >= 8) s *= 2;
     return s;
   }
-  const int bn = tile_n(N, epi);
+  const int bn = tile_n(N, K, epi);
   const int tiles = ((M + kBM - 1) / kBM) * ((N + bn - 1) / bn);
   const int steps = (K + kBK - 1) / kBK;
   int s = 1;
-  // Too few tiles leaves HBM idle: split K up to 4 ways until there are about
-  // two blocks per compute unit, keeping at least 8 K steps per block. The
-  // SiLU-gated GEMM is wide enough at decode batches and skips the extra pass.
-  // A narrow output has few tiles at any batch: split it up to 16 ways, down
-  // to 2 K steps per block.
+  // Too few tiles leaves HBM idle: split K up to 4 ways (8 for long K) until
+  // there are about two blocks per compute unit, keeping at least 8 K steps
+  // per block. The SiLU-gated GEMM is wide enough at decode batches and skips
+  // the extra pass. A narrow output has few tiles at any batch: split it up to
+  // 16 ways, down to 2 K steps per block.
   const int want = epi == EPI_SILU ? 256 : 512;
   const bool narrow = N <= 128;
-  const int max_s = narrow ? 16 : 4, min_steps = narrow ? 2 : 8;
+  const int max_s = narrow ? 16 : long_k(N, K, epi) ? 8 : 4, min_steps = narrow ? 2 : 8;
   while (tiles * s < want && s < max_s && steps / (s * 2) >= min_steps) s *= 2;
   return s;
 }

@@ -248,7 +248,7 @@ template <int EPI>
 hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
   const bool part = a.splits > 1;
   hipError_t e = part ? launch_stream<EPI, true>(a, s) : launch_stream<EPI, false>(a, s);
-  if (e != hipSuccess || !part) return e;
+  if (e != hipSuccess || !part || a.defer_reduce) return e;
   return launch_splitk_reduce(a, s);
 }
 

@@ -24,6 +24,7 @@ struct GemmArgs {
   int groups;
   int splits;                 // split-K count (>1: fp32 partials in `partial`, then a reduce)
   float *partial;
+  int defer_reduce;           // splits > 1: leave the partials for a consumer that sums them itself
 };
 
 // Compute units of the current device (queried once per process and device).
@@ -44,12 +45,15 @@ hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gain, uint16_t *out
                           float eps, hipStream_t s);
 
 // In-place RoPE of the q and k heads of qkv and/or append of k, v to the KV pool.
+// With splits > 1, each qkv row is first summed from the `splits` fp32 split-K
+// partials [splits][B][qkv width] (the same order and bf16 rounding as the
+// split-K reduce), so a qkv projection can hand its partials straight over.
 // ring > 0: page_table is a [B][ring] window-only page ring (logical page lp in
 // column lp % ring, contexts not clamped); max_pages is then ring.
 hipError_t launch_rope_append(uint16_t *qkv, int B, int n_q, int n_kv, int D, float theta,
                               const int32_t *ctx_lens, const int32_t *page_table, int max_pages, int ring,
                               uint16_t *pool, int64_t pool_pages, bool do_rope, bool do_append,
-                              hipStream_t s);
+                              hipStream_t s, const float *partial = nullptr, int splits = 1);
 
 // Paged GQA decode attention (the batch's pages split evenly over the waves)
 // + exact log-sum-exp merge of sequences that span several waves.

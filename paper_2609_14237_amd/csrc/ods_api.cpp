@@ -365,7 +365,8 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
     hipError_t e = hipSuccess;
     const char *what = kNames[k];
     GemmArgs ga{};
-    auto dense_gemm = [&](const void *A, const void *Bw, void *C, int N, int K, int epi, int n_up, int ldc) {
+    auto dense_gemm = [&](const void *A, const void *Bw, void *C, int N, int K, int epi, int n_up, int ldc,
+                          bool defer_reduce = false) {
       ga.A = (const uint16_t *)A; ga.lda = K;
       ga.B = (const uint16_t *)Bw; ga.ldb = K; ga.b_group_stride = 0;
       ga.C = C; ga.ldc = ldc;
@@ -373,12 +374,28 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
       ga.group_off = nullptr; ga.groups = 0;
       ga.splits = gemm_splits(B, N, K, epi);
       ga.partial = (float *)st->ws;
+      ga.defer_reduce = defer_reduce ? 1 : 0;
       return launch_gemm(ga, stream);
     };
     switch (k) {
       case K_ATTN_NORM: e = launch_rmsnorm(U(st->resid), U(L.g_attn), U(st->xn), B, H, c.rms_eps, stream); break;
       case K_FFN_NORM: e = launch_rmsnorm(U(st->resid), U(L.g_ffn), U(st->hn), B, H, c.rms_eps, stream); break;
-      case K_QKV: e = dense_gemm(st->xn, L.w_qkv, st->qkv, qkv_dim(c), H, EPI_BF16, 0, qkv_dim(c)); break;
+      case K_QKV: {
+        // With split-K and RoPE next in the range, the RoPE / KV-append kernel
+        // sums the partials itself (same order and rounding as the reduce).
+        const bool fuse = next_same_layer && ops[i + 1].kind == K_ROPE && gemm_splits(B, qkv_dim(c), H, EPI_BF16) > 1;
+        e = dense_gemm(st->xn, L.w_qkv, st->qkv, qkv_dim(c), H, EPI_BF16, 0, qkv_dim(c), fuse);
+        if (fuse && e == hipSuccess) {
+          const bool app = i + 2 < ops.size() && ops[i + 2].layer == ops[i].layer && ops[i + 2].kind == K_KV_APPEND;
+          const KvMap m = kv_map(c, batch);
+          e = launch_rope_append(U(st->qkv), B, c.n_q, c.n_kv, D, c.rope_theta, batch->ctx_lens, m.table, m.cols,
+                                 m.ring, U(L.kv_pool), L.pool_pages, true, app, stream, (const float *)st->ws,
+                                 ga.splits);
+          what = app ? "qkv_proj+rope+kv_append" : "qkv_proj+rope";
+          i += app ? 2 : 1;
+        }
+        break;
+      }
       case K_ROPE:
       case K_KV_APPEND: {
         const bool both = k == K_ROPE && next_same_layer && ops[i + 1].kind == K_KV_APPEND;

@@ -395,3 +395,37 @@ def test_layer_across_gemm_tile_paths(batch):
     torch.cuda.synchronize()
     assert_close("gu", f64(s.buf("gu", batch, 2 * cfg.ffn)), ref["gu"])
     assert_close("resid (split at silu)", f64(s.buf("resid", batch, cfg.hidden)), ref["resid"])
+
+
+# ---------------------------------------------------------------- fusions
+
+def test_qkv_split_reduce_fused_into_rope_is_bit_exact():
+    """With split-K on the qkv projection and RoPE in the same range, the RoPE /
+    KV-append kernel sums the partials itself. Same order, same rounding: the
+    fused range [0, 4) must leave qkv and the KV pool byte-identical to the
+    unfused cuts [0, 2) + [2, 4), and the layer must match the oracle."""
+    from paper_2609_14237_amd import binding as Bd
+    cfg = W.LayerCfg(hidden=2048, n_q=16, n_kv=4, head_dim=128, ffn=1024)
+    w = W.Workload("fused_qkv", (cfg,), batch=48, ctx_lo=1, ctx_hi=200)
+    assert Bd.lib.ods_workspace_bytes  # library loaded
+    say("qkv reduce fused into rope")
+    s = Setup(w, seed=31)
+    inp = s.oracle_inputs()
+    ref = oracle_run(fresh(inp), w.layers, 0, 10)
+    pool0 = s.pools[0].clone()
+    s.reset_resid()
+    s.run(0, 4)
+    torch.cuda.synchronize()
+    qkv_fused, pool_fused = s.buf("qkv", w.batch, cfg.qkv_dim).clone(), s.pools[0].clone()
+    s.pools[0].copy_(pool0)
+    s.reset_resid()
+    s.run(0, 2)
+    s.run(2, 4)
+    torch.cuda.synchronize()
+    assert torch.equal(s.buf("qkv", w.batch, cfg.qkv_dim), qkv_fused)
+    assert torch.equal(s.pools[0], pool_fused)
+    s.pools[0].copy_(pool0)
+    s.reset_resid()
+    s.run(0, 10)
+    torch.cuda.synchronize()
+    _check_layer_buffers(s, ref, cfg, w.batch)
