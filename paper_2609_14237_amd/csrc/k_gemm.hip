@@ -453,10 +453,17 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
   const int bn = tile_n(a.N, a.K, EPI);
   const int n_tiles = (a.N + bn - 1) / bn;
   if (a.group_off) {
-    // Expert row groups average B*k/E rows (64 at the MoE workload): a
-    // 128-row large-M tile covers a whole group, so each expert's weights
-    // stream once, and 128 weight rows per block keep the re-reads of the
-    // group's activations to one per 128 output columns.
+    // Expert row groups average B*k/E rows (64 at the MoE workload). The
+    // streaming kernel takes them when K is a whole number of 64-wide steps
+    // (one block per N tile and expert, the expert's rows in 256-row tiles).
+    if (a.K % 64 == 0) {
+      GemmArgs g = a;
+      g.splits = 1;
+      return launch_gemm_stream(g, s);
+    }
+    // Otherwise a 128-row large-M tile covers a whole group, so each expert's
+    // weights stream once, and 128 weight rows per block keep the re-reads of
+    // the group's activations to one per 128 output columns.
     const int bnb = EPI == EPI_SILU ? 64 : 128;
     dim3 grid((a.N + bnb - 1) / bnb, 1, a.groups);
     return launch_big<128, EPI, false>(a, grid, s);

@@ -1,9 +1,12 @@
 // Weight-streaming bf16 MFMA GEMM for M > 128 rows (the 256-row decode batch,
-// the 512-row MoE attention projections, larger prefill-sized batches):
+// the 512-row MoE attention projections, larger prefill-sized batches) and
+// for the grouped expert GEMMs (any rows per group):
 // C[m, n] = sum_k A[m, k] * B[n, k] with the same epilogues as the other
 // GEMM kernels. Built on its own with MFMA results in VGPRs (the build passes
 // -amdgpu-mfma-vgpr-form for this file only), which keeps the accumulators in
 // place across the K loop.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -58,36 +61,48 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
   uint8_t *const lds_b = (uint8_t *)smem;
   uint8_t *const lds_a = lds_b + NSLOT * BSTAGE + wm * NSLOT * ASTAGE;
 
-  // Blocks are dispatched to the 8 XCDs round-robin by index.
-  const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
-  const int g = 8 / p.splits;  // XCDs per K range
-  const int split = xcd / g;
-  const int mt = j % m_tiles, nt = (j / m_tiles) * g + xcd % g;
-  if (nt >= n_tiles) return;
-  const int n0 = nt * BN, m0 = mt * 256;
+  // The block's task: an N tile, a K range and the rows [m_first, m_last).
+  int nt, split = 0, m_first, m_last;
+  const uint16_t *Bg = p.B;
+  if (p.group_off) {
+    // Grouped (expert) GEMM: block (N tile, group g) over the group's rows,
+    // whatever their count, against weight slab g (no split-K).
+    nt = blockIdx.x;
+    const int gi = blockIdx.y;
+    m_first = max(0, p.group_off[gi]);      // offsets come from device memory:
+    m_last = min(p.M, p.group_off[gi + 1]);  // never step outside the M rows
+    Bg += (int64_t)gi * p.b_group_stride;
+    if (m_first >= m_last) return;
+  } else {
+    // Blocks are dispatched to the 8 XCDs round-robin by index.
+    const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
+    const int g = 8 / p.splits;  // XCDs per K range
+    split = xcd / g;
+    const int mt = j % m_tiles;
+    nt = (j / m_tiles) * g + xcd % g;
+    if (nt >= n_tiles) return;
+    m_first = mt * 256;
+    m_last = min(p.M, m_first + 256);
+  }
+  const int n0 = nt * BN;
 
   const int steps = p.K / BK;
   const int per = (steps + p.splits - 1) / p.splits;
   const int s_begin = split * per;
   const int nk = min(per, steps - s_begin);  // may be <= 0 for a trailing split: it writes zeros
+  const int last = max(nk - 1, 0);
 
   // Load q fills LDS row 8q + lane / 8 of its tile, position lane % 8, with
   // chunk c = (lane % 8) ^ (row % 8) of that row, so chunk c of row r sits at
-  // position c ^ (r % 8). A rows past M re-read row M - 1 and are never stored.
+  // position c ^ (r % 8).
   const int chunk = ((lane & 7) ^ (lane >> 3)) * 8;
-  const uint16_t *aptr[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int m = min(m0 + wm * 64 + (wn * 4 + q) * 8 + (lane >> 3), p.M - 1);
-    aptr[q] = p.A + (int64_t)m * p.lda + (int64_t)s_begin * BK + chunk;
-  }
   const uint16_t *bptr[2];
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const int r = (wave * 2 + q) * 8 + (lane >> 3);
     const int n = min(n0 + (SILU ? r % BN : r), p.N - 1);
     const int row = SILU && r >= BN ? p.n_up + n : n;
-    bptr[q] = p.B + (int64_t)row * p.ldb + (int64_t)s_begin * BK + chunk;
+    bptr[q] = Bg + (int64_t)row * p.ldb + (int64_t)s_begin * BK + chunk;
   }
   // Fragment read: row 16i + lane % 16, chunk 4 ks + lane / 16. B tile row of
   // fragment jt: SiLU takes gate rows 32 wn + 16 jt (jt < 2) and the matching up
@@ -96,130 +111,153 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
   const int rd_off1 = (lane & 15) * 128 + (((4 + (lane >> 4)) ^ (lane & 7)) << 4);
   auto brow = [&](int jt) { return SILU ? (jt >> 1) * 64 + wn * 32 + (jt & 1) * 16 : wn * 64 + jt * 16; };
 
-  f32x4 acc[4][TN];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int jt = 0; jt < TN; ++jt) acc[i][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const int last = max(nk - 1, 0);
-  auto issue = [&](int t, int slot) {
-    const int64_t k = (int64_t)min(t, last) * BK;
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      __builtin_amdgcn_global_load_lds(
-          (const void *)(aptr[q] + k),
-          (__attribute__((address_space(3))) void *)(lds_a + slot * ASTAGE + (wn * 4 + q) * 1024), 16, 0, 0);
-#pragma unroll
-    for (int q = 0; q < 2; ++q)
-      __builtin_amdgcn_global_load_lds(
-          (const void *)(bptr[q] + k),
-          (__attribute__((address_space(3))) void *)(lds_b + slot * BSTAGE + (wave * 2 + q) * 1024), 16, 0, 0);
-  };
   // Fragments of one K step: A row groups i and B fragments jt, both K halves.
   struct Frags {
     bf16x8 a[2][4], b[2][TN];
   };
-  auto read_frags = [&](Frags &f, int slot) {
-    const uint8_t *as = lds_a + slot * ASTAGE, *bs = lds_b + slot * BSTAGE;
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int off = ks ? rd_off1 : rd_off0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) f.a[ks][i] = __builtin_bit_cast(bf16x8, *(const u32x4 *)(as + i * 2048 + off));
-#pragma unroll
-      for (int jt = 0; jt < TN; ++jt)
-        f.b[ks][jt] = __builtin_bit_cast(bf16x8, *(const u32x4 *)(bs + brow(jt) * 128 + off));
-    }
-  };
-  auto mma = [&](const Frags &f) {
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int jt = 0; jt < TN; ++jt) acc[i][jt] = mfma_16x16x32(f.a[ks][i], f.b[ks][jt], acc[i][jt]);
-  };
+  f32x4 acc[4][TN];
 
-  if (nk > 0) {
-    // Step t runs its MFMAs on fragments read during step t - 1, reads the
-    // fragments of step t + 1, and refills the slot of step t (free once its
-    // fragments are in registers) with the loads of step t + 3.
-    issue(0, 0);
-    issue(1, 1);
-    issue(2, 2);
-    Frags f0, f1;
-    __builtin_amdgcn_sched_barrier(0);
-    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * LOADS) : "memory");
-    __builtin_amdgcn_sched_barrier(0);
-    read_frags(f0, 0);
-    int slot = 0;  // slot of step t
-    auto step = [&](int t, const Frags &cur, Frags &nxt) {
-      // Loads of step t + 1 have landed once only those of step t + 2 are
-      // outstanding; lgkmcnt(0) retires this wave's reads of slot t (issued a
-      // step ago) before the barrier lets step t + 3 overwrite it.
-      __builtin_amdgcn_sched_barrier(0);
-      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LOADS) : "memory");
-      __builtin_amdgcn_sched_barrier(0);
-      const int s1 = slot == NSLOT - 1 ? 0 : slot + 1;
-      issue(t + 3, slot);
-      read_frags(nxt, s1);
-      mma(cur);
-      // Interleave one global load per MFMA, then one fragment read per MFMA,
-      // then the rest of the MFMAs. Loads issued in one burst by all eight
-      // waves back up the address unit and stall the issuing waves; reads
-      // issued in one burst ahead of the MFMAs make the compiler drain them
-      // all (lgkmcnt counts only to 15) before the first MFMA.
+  for (int m0 = m_first; m0 < m_last; m0 += 256) {
+    // A rows past the tile's last row re-read that row and are never stored.
+    const uint16_t *aptr[4];
 #pragma unroll
-      for (int k = 0; k < LOADS; ++k) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      }
+    for (int q = 0; q < 4; ++q) {
+      const int m = min(m0 + wm * 64 + (wn * 4 + q) * 8 + (lane >> 3), m_last - 1);
+      aptr[q] = p.A + (int64_t)m * p.lda + (int64_t)s_begin * BK + chunk;
+    }
 #pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int jt = 0; jt < TN; ++jt) acc[i][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // Waves whose 64 rows all lie past the tile's end (a short expert group)
+    // only load their share of B; they issue fewer loads per step, so they
+    // wait for their own count. Every wave passes the same barriers.
+    const bool live = m0 + wm * 64 < m_last;
+    auto pipeline = [&](auto live_c) {
+      constexpr bool LIVE = decltype(live_c)::value;
+      constexpr int LW = LIVE ? LOADS : 2;  // loads per step of this wave
+      auto issue = [&](int t, int slot) {
+        const int64_t k = (int64_t)min(t, last) * BK;
+        if (LIVE) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            __builtin_amdgcn_global_load_lds(
+                (const void *)(aptr[q] + k),
+                (__attribute__((address_space(3))) void *)(lds_a + slot * ASTAGE + (wn * 4 + q) * 1024), 16, 0, 0);
+        }
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+          __builtin_amdgcn_global_load_lds(
+              (const void *)(bptr[q] + k),
+              (__attribute__((address_space(3))) void *)(lds_b + slot * BSTAGE + (wave * 2 + q) * 1024), 16, 0, 0);
+      };
+      auto read_frags = [&](Frags &f, int slot) {
+        const uint8_t *as = lds_a + slot * ASTAGE, *bs = lds_b + slot * BSTAGE;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const int off = ks ? rd_off1 : rd_off0;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) f.a[ks][i] = __builtin_bit_cast(bf16x8, *(const u32x4 *)(as + i * 2048 + off));
+#pragma unroll
+          for (int jt = 0; jt < TN; ++jt)
+            f.b[ks][jt] = __builtin_bit_cast(bf16x8, *(const u32x4 *)(bs + brow(jt) * 128 + off));
+        }
+      };
+      auto mma = [&](const Frags &f) {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int jt = 0; jt < TN; ++jt) acc[i][jt] = mfma_16x16x32(f.a[ks][i], f.b[ks][jt], acc[i][jt]);
+      };
+      // Step t runs its MFMAs on fragments read during step t - 1, reads the
+      // fragments of step t + 1, and refills the slot of step t (free once its
+      // fragments are in registers) with the loads of step t + 3.
+      issue(0, 0);
+      issue(1, 1);
+      issue(2, 2);
+      Frags f0, f1;
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * LW) : "memory");
+      __builtin_amdgcn_sched_barrier(0);
+      if (LIVE) read_frags(f0, 0);
+      int slot = 0;  // slot of step t
+      auto step = [&](int t, const Frags &cur, Frags &nxt) {
+        // Loads of step t + 1 have landed once only those of step t + 2 are
+        // outstanding; lgkmcnt(0) retires this wave's reads of slot t (issued
+        // a step ago) before the barrier lets step t + 3 overwrite it.
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LW) : "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        const int s1 = slot == NSLOT - 1 ? 0 : slot + 1;
+        issue(t + 3, slot);
+        if (LIVE) {
+          read_frags(nxt, s1);
+          mma(cur);
+          // Interleave one global load per MFMA, then one fragment read per
+          // MFMA, then the rest of the MFMAs. Loads issued in one burst by all
+          // eight waves back up the address unit and stall the issuing waves;
+          // reads issued in one burst ahead of the MFMAs make the compiler
+          // drain them all (lgkmcnt counts only to 15) before the first MFMA.
+#pragma unroll
+          for (int k = 0; k < LOADS; ++k) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+          }
+#pragma unroll
+          for (int k = 0; k < 16; ++k) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, 32 - LOADS - 16, 0);
+        }
+        slot = s1;
+      };
+      int t = 0;
+      for (; t + 2 <= nk; t += 2) {
+        step(t, f0, f1);
+        step(t + 1, f1, f0);
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, 32 - LOADS - 16, 0);
-      slot = s1;
+      if (t < nk) step(t, f0, f1);
+      // Nothing may still be writing the LDS slots when they are reused or the block retires.
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
     };
-    int t = 0;
-    for (; t + 2 <= nk; t += 2) {
-      step(t, f0, f1);
-      step(t + 1, f1, f0);
+    if (nk > 0) {
+      if (live) pipeline(std::true_type{});
+      else pipeline(std::false_type{});
     }
-    if (t < nk) step(t, f0, f1);
-    // Nothing may still be writing this block's LDS when it retires.
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  }
+    if (!live) continue;
 
-  // Epilogue: lane holds rows (lane >> 4) * 4 + e of column lane & 15 of each 16x16 tile.
-  constexpr int TO = SILU ? TN / 2 : TN;  // output fragments (SiLU pairs gate jt with up jt + TO)
+    // Epilogue: lane holds rows (lane >> 4) * 4 + e of column lane & 15 of each 16x16 tile.
+    constexpr int TO = SILU ? TN / 2 : TN;  // output fragments (SiLU pairs gate jt with up jt + TO)
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 4; ++i) {
 #pragma unroll
-    for (int jt = 0; jt < TO; ++jt) {
-      const int n = n0 + (SILU ? wn * 32 : wn * 64) + jt * 16 + (lane & 15);
-      if (n >= p.N) continue;
+      for (int jt = 0; jt < TO; ++jt) {
+        const int n = n0 + (SILU ? wn * 32 : wn * 64) + jt * 16 + (lane & 15);
+        if (n >= p.N) continue;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + e;
-        if (m >= p.M) continue;
-        const float v = acc[i][jt][e];
-        if (PARTIAL) {
-          const int64_t ncols = SILU ? 2 * (int64_t)p.N : p.N;
-          float *dst = p.partial + ((int64_t)split * p.M + m) * ncols;
-          dst[n] = v;
-          if (SILU) dst[p.N + n] = acc[i][jt + TO][e];
-        } else if (EPI == EPI_BF16) {
-          ((uint16_t *)p.C)[(int64_t)m * p.ldc + n] = f2bf(v);
-        } else if (EPI == EPI_F32) {
-          ((float *)p.C)[(int64_t)m * p.ldc + n] = v;
-        } else if (EPI == EPI_RESID) {
-          uint16_t *c = (uint16_t *)p.C + (int64_t)m * p.ldc + n;
-          *c = f2bf(bf2f(*c) + v);
-        } else {
-          ((uint16_t *)p.C)[(int64_t)m * p.ldc + n] = f2bf(silu(v) * acc[i][jt + TO][e]);
+        for (int e = 0; e < 4; ++e) {
+          const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + e;
+          if (m >= m_last) continue;
+          const float v = acc[i][jt][e];
+          if (PARTIAL) {
+            const int64_t ncols = SILU ? 2 * (int64_t)p.N : p.N;
+            float *dst = p.partial + ((int64_t)split * p.M + m) * ncols;
+            dst[n] = v;
+            if (SILU) dst[p.N + n] = acc[i][jt + TO][e];
+          } else if (EPI == EPI_BF16) {
+            ((uint16_t *)p.C)[(int64_t)m * p.ldc + n] = f2bf(v);
+          } else if (EPI == EPI_F32) {
+            ((float *)p.C)[(int64_t)m * p.ldc + n] = v;
+          } else if (EPI == EPI_RESID) {
+            uint16_t *c = (uint16_t *)p.C + (int64_t)m * p.ldc + n;
+            *c = f2bf(bf2f(*c) + v);
+          } else {
+            ((uint16_t *)p.C)[(int64_t)m * p.ldc + n] = f2bf(silu(v) * acc[i][jt + TO][e]);
+          }
         }
       }
     }
@@ -231,7 +269,8 @@ hipError_t launch_stream(const GemmArgs &a, hipStream_t s) {
   constexpr int BN = EPI == EPI_SILU ? 64 : 128;
   const int n_tiles = (a.N + BN - 1) / BN, m_tiles = (a.M + 255) / 256;
   const int g = 8 / a.splits;  // splits is 1, 2, 4 or 8 (gemm_stream_splits)
-  const int blocks = 8 * m_tiles * ((n_tiles + g - 1) / g);
+  // dense: a 1-D grid placed on the XCDs; grouped: (N tile, group)
+  const dim3 grid = a.group_off ? dim3(n_tiles, a.groups) : dim3(8 * m_tiles * ((n_tiles + g - 1) / g));
   auto kern = gemm_stream_kernel<EPI, PARTIAL>;
   const size_t lds = (size_t)3 * 128 * 64 * 2 + 4 * 3 * 64 * 64 * 2;  // 3 B slots + 3 A slots per M group
   static bool attr_set = false;  // the attribute only raises a per-kernel limit; setting it twice is harmless
@@ -240,7 +279,7 @@ hipError_t launch_stream(const GemmArgs &a, hipStream_t s) {
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(512), lds, s, a, n_tiles, m_tiles);
+  hipLaunchKernelGGL(kern, grid, dim3(512), lds, s, a, n_tiles, m_tiles);
   return hipGetLastError();
 }
 
@@ -270,6 +309,7 @@ int gemm_stream_splits(int M, int N, int K, int epi) {
 
 hipError_t launch_gemm_stream(const GemmArgs &a, hipStream_t s) {
   if (a.splits != 1 && a.splits != 2 && a.splits != 4 && a.splits != 8) return hipErrorInvalidValue;
+  if (a.group_off && (a.splits != 1 || a.groups <= 0)) return hipErrorInvalidValue;
   switch (a.epi) {
     case EPI_BF16: return launch_epi<EPI_BF16>(a, s);
     case EPI_F32: return launch_epi<EPI_F32>(a, s);
