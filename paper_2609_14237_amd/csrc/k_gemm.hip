@@ -7,8 +7,10 @@
 // on the matrix cores). Decode GEMMs are weight-streaming (M <= 64 rows against
 // megabytes of weights), so the tile covers all rows it can and narrow outputs
 // are split along K to keep every compute unit streaming. Dense GEMMs past 128
-// rows go to the direct-to-LDS streaming kernel (k_gemm_stream.hip); the
-// large-M kernel here takes 64 < M <= 128 and the grouped expert GEMMs. MFMA 16x16x32 bf16: lane l holds A[m = l%16][8 k's
+// rows, those of 33 to 64 rows but the SiLU-gated one, and the grouped expert
+// GEMMs with K % 64 = 0 go to the direct-to-LDS streaming kernel
+// (k_gemm_stream.hip); the large-M kernel here takes 64 < M <= 128 and the
+// grouped GEMMs with other K. MFMA 16x16x32 bf16: lane l holds A[m = l%16][8 k's
 // starting at (l/16)*8] and B[same k's][n = l%16]; the 16x16 fp32 result puts
 // rows (l/16)*4 .. +3 of column l%16 in lane l.
 #include "common.hpp"
@@ -455,7 +457,8 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
   if (a.group_off) {
     // Expert row groups average B*k/E rows (64 at the MoE workload). The
     // streaming kernel takes them when K is a whole number of 64-wide steps
-    // (one block per N tile and expert, the expert's rows in 256-row tiles).
+    // (one block per N tile and expert, the expert's rows in 64- or 256-row
+    // tiles).
     if (a.K % 64 == 0) {
       GemmArgs g = a;
       g.splits = 1;
@@ -470,7 +473,7 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
   }
   const bool part = a.splits > 1;
   hipError_t e;
-  if (gemm_use_stream(a.M, a.N, a.K)) return launch_gemm_stream(a, s);  // launches its own reduce
+  if (gemm_use_stream(a.M, a.N, a.K, EPI)) return launch_gemm_stream(a, s);  // launches its own reduce
   if (use_big(a.M, a.N)) {
     const int bm = a.M > 128 ? 256 : 128;
     const int bnb = EPI == EPI_SILU ? 64 : 128;
@@ -494,7 +497,7 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
 }  // namespace
 
 int gemm_splits(int M, int N, int K, int epi) {
-  if (gemm_use_stream(M, N, K)) return gemm_stream_splits(M, N, K, epi);
+  if (gemm_use_stream(M, N, K, epi)) return gemm_stream_splits(M, N, K, epi);
   if (N % 4 != 0) return 1;  // the reduce works on 4-column groups
   if (use_big(M, N)) {
     // Large-M tiles: one 512-thread block per compute unit; split K (up to 8

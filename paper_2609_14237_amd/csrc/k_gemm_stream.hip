@@ -1,10 +1,11 @@
 // Weight-streaming bf16 MFMA GEMM for M > 128 rows (the 256-row decode batch,
-// the 512-row MoE attention projections, larger prefill-sized batches) and
-// for the grouped expert GEMMs (any rows per group):
-// C[m, n] = sum_k A[m, k] * B[n, k] with the same epilogues as the other
-// GEMM kernels. Built on its own with MFMA results in VGPRs (the build passes
-// -amdgpu-mfma-vgpr-form for this file only), which keeps the accumulators in
-// place across the K loop.
+// the 512-row MoE attention projections, larger prefill-sized batches), for
+// 33 to 64 rows outside the SiLU-gated FFN GEMM, and for the grouped expert
+// GEMMs (any rows per group): C[m, n] = sum_k A[m, k] * B[n, k] with the same
+// epilogues as the other GEMM kernels. Built on its own with MFMA results in
+// VGPRs (the build passes -amdgpu-mfma-vgpr-form for this file only), which
+// keeps the accumulators in place across the K loop.
+#include <cstdlib>
 #include <type_traits>
 
 #include "common.hpp"
@@ -14,22 +15,24 @@ namespace ods {
 
 namespace {
 
-// Weight-streaming variant for M > 128 (K % 64 == 0): 512 threads = 8 waves,
-// two per SIMD, as 4 (M) x 2 (N); a block owns a 256-row tile of A and 128
-// rows of B (SiLU: 64 gate + 64 up rows, each wave taking 32 of each so gate
-// and up of an output column meet in one lane). Wave (wm, wn) computes rows
-// [64 wm, 64 wm + 64) against its 64 B rows.
+// Two tile shapes (K % 64 == 0), both with two waves per SIMD and 128 rows of
+// B per block (SiLU: 64 gate + 64 up rows, each wave taking the gate and up
+// rows of the same output columns, so both halves of a column meet in one
+// lane). MG = 4: 512 threads = 8 waves as 4 (M) x 2 (N) over a 256-row tile of
+// A, 144 KB of LDS, one block per CU. MG = 1: 256 threads = 4 waves as 1 x 4
+// over a 64-row tile, 72 KB, two blocks per CU. Wave (wm, wn) computes rows
+// [64 wm, 64 wm + 64) against its 128 / WN rows of B.
 //
 // Both operands go from global memory straight into LDS (direct-to-LDS loads:
 // no registers and no LDS store instructions), eight lanes per 128-byte row
 // segment so every load reads whole cache lines. A load writes its 64 lanes'
 // 16 bytes in lane order; choosing which chunk each lane fetches XOR-swizzles
 // the chunks of each row by row index, so the MFMA fragment reads are
-// conflict-free. A rows land in an area per M group (shared by its two
+// conflict-free. A rows land in an area per M group (shared by that group's
 // waves), B rows in an area all waves share; both are rings of three K steps,
 // filled two steps ahead. Two waves per SIMD matter: one wave per SIMD draws
-// about 25 B/clk from LDS, two about 50, and each wave reads 16 KB of
-// fragments per K step.
+// about 25 B/clk from LDS, two about 50, and each wave reads 16 KB (MG = 4)
+// or 12 KB (MG = 1) of fragments per K step.
 //
 // Synchronisation is explicit: the only vector-memory instructions in the
 // loop are these loads (one event type, completed in order), so at the top of
@@ -43,21 +46,24 @@ namespace {
 // (split-K) and the M tiles of one weight slab run on one XCD at the same
 // time, so A slices and weight slabs are served by that XCD's L2. This file
 // is built with MFMA results in VGPRs, which keeps the accumulators in place.
-template <int EPI, bool PARTIAL>
-__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+// MG = 64-row M groups per block (4 or 1, above).
+template <int MG, int EPI, bool PARTIAL>
+__global__ __launch_bounds__(MG == 4 ? 512 : 256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
   constexpr int BK = 64, NSLOT = 3, BNR = 128;
+  constexpr int WN = MG == 4 ? 2 : 4, WAVES = MG * WN, BM = 64 * MG;
   constexpr bool SILU = EPI == EPI_SILU;
   constexpr int BN = SILU ? BNR / 2 : BNR;  // output columns per block
-  constexpr int TN = 4;                     // B fragments per wave and K half
-  constexpr int LOADS = 4 + 2;              // loads per wave per step: half an M group's A, 1/8 of B
+  constexpr int TN = 8 / WN;                // B fragments per wave and K half
+  constexpr int AL = 8 / WN, BL = 16 / WAVES;
+  constexpr int LOADS = AL + BL;            // loads per wave per step: its part of an M group's A and of B
   constexpr int BSTAGE = BNR * BK * 2;      // bytes of one B tile (16 KB)
   constexpr int ASTAGE = 64 * BK * 2;       // bytes of one M group's A tile (8 KB)
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];  // B slots, then A slots per M group
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   uint8_t *const lds_b = (uint8_t *)smem;
   uint8_t *const lds_a = lds_b + NSLOT * BSTAGE + wm * NSLOT * ASTAGE;
 
@@ -81,8 +87,8 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
     const int mt = j % m_tiles;
     nt = (j / m_tiles) * g + xcd % g;
     if (nt >= n_tiles) return;
-    m_first = mt * 256;
-    m_last = min(p.M, m_first + 256);
+    m_first = mt * BM;
+    m_last = min(p.M, m_first + BM);
   }
   const int n0 = nt * BN;
 
@@ -96,20 +102,23 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
   // chunk c = (lane % 8) ^ (row % 8) of that row, so chunk c of row r sits at
   // position c ^ (r % 8).
   const int chunk = ((lane & 7) ^ (lane >> 3)) * 8;
-  const uint16_t *bptr[2];
+  const uint16_t *bptr[BL];
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int r = (wave * 2 + q) * 8 + (lane >> 3);
+  for (int q = 0; q < BL; ++q) {
+    const int r = (wave * BL + q) * 8 + (lane >> 3);
     const int n = min(n0 + (SILU ? r % BN : r), p.N - 1);
     const int row = SILU && r >= BN ? p.n_up + n : n;
     bptr[q] = Bg + (int64_t)row * p.ldb + (int64_t)s_begin * BK + chunk;
   }
   // Fragment read: row 16i + lane % 16, chunk 4 ks + lane / 16. B tile row of
-  // fragment jt: SiLU takes gate rows 32 wn + 16 jt (jt < 2) and the matching up
-  // rows 64 + 32 wn + 16 (jt - 2), so gate fragment jt pairs with up fragment jt + 2.
+  // fragment jt: SiLU takes gate rows (64 / WN) wn + 16 jt (jt < TN / 2) and the
+  // matching up rows 64 + (64 / WN) wn + 16 (jt - TN / 2), so gate fragment jt
+  // pairs with up fragment jt + TN / 2.
   const int rd_off0 = (lane & 15) * 128 + (((lane >> 4) ^ (lane & 7)) << 4);
   const int rd_off1 = (lane & 15) * 128 + (((4 + (lane >> 4)) ^ (lane & 7)) << 4);
-  auto brow = [&](int jt) { return SILU ? (jt >> 1) * 64 + wn * 32 + (jt & 1) * 16 : wn * 64 + jt * 16; };
+  auto brow = [&](int jt) {
+    return SILU ? (jt / (TN / 2)) * 64 + wn * (64 / WN) + (jt % (TN / 2)) * 16 : wn * (128 / WN) + jt * 16;
+  };
 
   // Fragments of one K step: A row groups i and B fragments jt, both K halves.
   struct Frags {
@@ -117,12 +126,12 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
   };
   f32x4 acc[4][TN];
 
-  for (int m0 = m_first; m0 < m_last; m0 += 256) {
+  for (int m0 = m_first; m0 < m_last; m0 += BM) {
     // A rows past the tile's last row re-read that row and are never stored.
-    const uint16_t *aptr[4];
+    const uint16_t *aptr[AL];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int m = min(m0 + wm * 64 + (wn * 4 + q) * 8 + (lane >> 3), m_last - 1);
+    for (int q = 0; q < AL; ++q) {
+      const int m = min(m0 + wm * 64 + (wn * AL + q) * 8 + (lane >> 3), m_last - 1);
       aptr[q] = p.A + (int64_t)m * p.lda + (int64_t)s_begin * BK + chunk;
     }
 #pragma unroll
@@ -136,21 +145,21 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
     const bool live = m0 + wm * 64 < m_last;
     auto pipeline = [&](auto live_c) {
       constexpr bool LIVE = decltype(live_c)::value;
-      constexpr int LW = LIVE ? LOADS : 2;  // loads per step of this wave
+      constexpr int LW = LIVE ? LOADS : BL;  // loads per step of this wave
       auto issue = [&](int t, int slot) {
         const int64_t k = (int64_t)min(t, last) * BK;
         if (LIVE) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
+          for (int q = 0; q < AL; ++q)
             __builtin_amdgcn_global_load_lds(
                 (const void *)(aptr[q] + k),
-                (__attribute__((address_space(3))) void *)(lds_a + slot * ASTAGE + (wn * 4 + q) * 1024), 16, 0, 0);
+                (__attribute__((address_space(3))) void *)(lds_a + slot * ASTAGE + (wn * AL + q) * 1024), 16, 0, 0);
         }
 #pragma unroll
-        for (int q = 0; q < 2; ++q)
+        for (int q = 0; q < BL; ++q)
           __builtin_amdgcn_global_load_lds(
               (const void *)(bptr[q] + k),
-              (__attribute__((address_space(3))) void *)(lds_b + slot * BSTAGE + (wave * 2 + q) * 1024), 16, 0, 0);
+              (__attribute__((address_space(3))) void *)(lds_b + slot * BSTAGE + (wave * BL + q) * 1024), 16, 0, 0);
       };
       auto read_frags = [&](Frags &f, int slot) {
         const uint8_t *as = lds_a + slot * ASTAGE, *bs = lds_b + slot * BSTAGE;
@@ -201,17 +210,19 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
           // eight waves back up the address unit and stall the issuing waves;
           // reads issued in one burst ahead of the MFMAs make the compiler
           // drain them all (lgkmcnt counts only to 15) before the first MFMA.
+          constexpr int NM = 8 * TN, NR = 8 + 2 * TN;  // MFMAs and fragment reads per step
+          constexpr int NMR = NR < NM - LOADS ? NR : NM - LOADS;
 #pragma unroll
           for (int k = 0; k < LOADS; ++k) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
           }
 #pragma unroll
-          for (int k = 0; k < 16; ++k) {
+          for (int k = 0; k < NMR; ++k) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
           }
-          __builtin_amdgcn_sched_group_barrier(0x008, 32 - LOADS - 16, 0);
+          if (NM - LOADS - NMR > 0) __builtin_amdgcn_sched_group_barrier(0x008, NM - LOADS - NMR, 0);
         }
         slot = s1;
       };
@@ -236,7 +247,7 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
       for (int jt = 0; jt < TO; ++jt) {
-        const int n = n0 + (SILU ? wn * 32 : wn * 64) + jt * 16 + (lane & 15);
+        const int n = n0 + (SILU ? wn * (64 / WN) : wn * (128 / WN)) + jt * 16 + (lane & 15);
         if (n >= p.N) continue;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -264,36 +275,58 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
   }
 }
 
-template <int EPI, bool PARTIAL>
+template <int MG, int EPI, bool PARTIAL>
 hipError_t launch_stream(const GemmArgs &a, hipStream_t s) {
   constexpr int BN = EPI == EPI_SILU ? 64 : 128;
-  const int n_tiles = (a.N + BN - 1) / BN, m_tiles = (a.M + 255) / 256;
+  const int n_tiles = (a.N + BN - 1) / BN, m_tiles = (a.M + 64 * MG - 1) / (64 * MG);
   const int g = 8 / a.splits;  // splits is 1, 2, 4 or 8 (gemm_stream_splits)
   // dense: a 1-D grid placed on the XCDs; grouped: (N tile, group)
   const dim3 grid = a.group_off ? dim3(n_tiles, a.groups) : dim3(8 * m_tiles * ((n_tiles + g - 1) / g));
-  auto kern = gemm_stream_kernel<EPI, PARTIAL>;
-  const size_t lds = (size_t)3 * 128 * 64 * 2 + 4 * 3 * 64 * 64 * 2;  // 3 B slots + 3 A slots per M group
+  auto kern = gemm_stream_kernel<MG, EPI, PARTIAL>;
+  const size_t lds = (size_t)3 * 128 * 64 * 2 + MG * 3 * 64 * 64 * 2;  // 3 B slots + 3 A slots per M group
   static bool attr_set = false;  // the attribute only raises a per-kernel limit; setting it twice is harmless
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, grid, dim3(512), lds, s, a, n_tiles, m_tiles);
+  hipLaunchKernelGGL(kern, grid, dim3(MG == 4 ? 512 : 256), lds, s, a, n_tiles, m_tiles);
   return hipGetLastError();
+}
+
+// 64-row tiles (two blocks per CU) for batches of at most 64 rows and for
+// expert groups of at most 32 rows on average; 256-row tiles otherwise. With
+// about 64 rows per expert (the binomial spread puts half the experts above
+// 64) the 64-row tile needs a second pass over the weights for those experts:
+// 745 against 588 us for the expert GEMMs of a 512-token batch over 64
+// experts, top 8. ODS_STREAM_SMALL=0/1 forces one or the other (measurements).
+bool gemm_stream_small_tile(const GemmArgs &a) {
+  static const int force = getenv("ODS_STREAM_SMALL") ? atoi(getenv("ODS_STREAM_SMALL")) : -1;
+  if (force >= 0) return force == 1;
+  if (a.group_off) return a.groups > 0 && a.M <= 32 * a.groups;
+  return a.M <= 64;
 }
 
 template <int EPI>
 hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
   const bool part = a.splits > 1;
-  hipError_t e = part ? launch_stream<EPI, true>(a, s) : launch_stream<EPI, false>(a, s);
+  const bool small = gemm_stream_small_tile(a);
+  hipError_t e = small ? (part ? launch_stream<1, EPI, true>(a, s) : launch_stream<1, EPI, false>(a, s))
+                       : (part ? launch_stream<4, EPI, true>(a, s) : launch_stream<4, EPI, false>(a, s));
   if (e != hipSuccess || !part || a.defer_reduce) return e;
   return launch_splitk_reduce(a, s);
 }
 
 }  // namespace
 
-bool gemm_use_stream(int M, int N, int K) { return M > 128 && N > 128 && K % 64 == 0; }
+// Dense GEMMs past 128 rows, and those of 33 to 64 rows except the SiLU-gated
+// one (64-row tiles: at 64 rows qkv 20.2 -> 18.0 us, o_proj 16.4 -> 15.9 us and
+// down 31.8 -> 29.2 us on the 8B-shaped layer, gate_up level at 53 us and
+// slower below 48 rows; at 32 rows and fewer the gains are under 1 us).
+bool gemm_use_stream(int M, int N, int K, int epi) {
+  if (N <= 128 || K % 64 != 0) return false;
+  return M > 128 || (M > 32 && M <= 64 && epi != EPI_SILU);
+}
 
 // Split K (1, 2, 4 or 8 ways, at least 8 steps per split) until about 192
 // blocks are in flight; the reduce works on 4-column groups.

@@ -37,7 +37,7 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
 // Sum of split-K partials plus the epilogue (after a partial-writing launch).
 hipError_t launch_splitk_reduce(const GemmArgs &a, hipStream_t s);
 // Weight-streaming kernel for dense GEMMs past 128 rows (K % 64 == 0).
-bool gemm_use_stream(int M, int N, int K);
+bool gemm_use_stream(int M, int N, int K, int epi);
 int gemm_stream_splits(int M, int N, int K, int epi);
 hipError_t launch_gemm_stream(const GemmArgs &a, hipStream_t s);
 

@@ -397,6 +397,30 @@ def test_layer_across_gemm_tile_paths(batch):
     assert_close("resid (split at silu)", f64(s.buf("resid", batch, cfg.hidden)), ref["resid"])
 
 
+@pytest.mark.parametrize("batch", [33, 47, 64])
+def test_layer_on_64_row_stream_tiles(batch):
+    """33 to 64 rows send qkv, o_proj and down (K a multiple of 64) to the
+    64-row streaming tile; H = 704 and qkv N = 832 leave N tails of the
+    128-column tile, and split-K partials are reduced both fused into RoPE
+    (qkv) and on their own (o_proj, down)."""
+    cfg = W.LayerCfg(hidden=704, n_q=11, n_kv=1, head_dim=64, ffn=768)
+    w = W.Workload("stream64", (cfg,), batch=batch, ctx_lo=1, ctx_hi=90)
+    say("64-row stream tiles, batch", batch)
+    s = Setup(w, seed=21)
+    inp = s.oracle_inputs()
+    ref = oracle_run(fresh(inp), w.layers, 0, 10)
+    s.reset_resid()
+    s.run(0, 10)
+    torch.cuda.synchronize()
+    _check_layer_buffers(s, ref, cfg, batch)
+    # every stage boundary: the unfused qkv and o_proj outputs
+    s.reset_resid()
+    for a, b in [(0, 2), (2, 3), (3, 5), (5, 6), (6, 10)]:
+        s.run(a, b)
+    torch.cuda.synchronize()
+    _check_layer_buffers(s, ref, cfg, batch)
+
+
 # ---------------------------------------------------------------- fusions
 
 def test_qkv_split_reduce_fused_into_rope_is_bit_exact():
