@@ -5,7 +5,6 @@
 // epilogues as the other GEMM kernels. Built on its own with MFMA results in
 // VGPRs (the build passes -amdgpu-mfma-vgpr-form for this file only), which
 // keeps the accumulators in place across the K loop.
-#include <cstdlib>
 #include <type_traits>
 
 #include "common.hpp"
@@ -299,10 +298,8 @@ hipError_t launch_stream(const GemmArgs &a, hipStream_t s) {
 // about 64 rows per expert (the binomial spread puts half the experts above
 // 64) the 64-row tile needs a second pass over the weights for those experts:
 // 745 against 588 us for the expert GEMMs of a 512-token batch over 64
-// experts, top 8. ODS_STREAM_SMALL=0/1 forces one or the other (measurements).
+// experts, top 8.
 bool gemm_stream_small_tile(const GemmArgs &a) {
-  static const int force = getenv("ODS_STREAM_SMALL") ? atoi(getenv("ODS_STREAM_SMALL")) : -1;
-  if (force >= 0) return force == 1;
   if (a.group_off) return a.groups > 0 && a.M <= 32 * a.groups;
   return a.M <= 64;
 }
