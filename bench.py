@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--workload", default="dense8b_b64")
     ap.add_argument("--copies", type=int, default=0, help="weight/KV copies in rotation (0: auto)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--weights", choices=("tiled", "rows"), default="tiled",
+                    help="projection weight layout: tiled (converted once at setup, the streaming GEMM's "
+                         "tile order) or row-major; tiled falls back to rows for shapes it does not take")
     ap.add_argument("--swa-ring", action="store_true",
                     help="sliding-window layers keep their KV in a window-only page ring "
                          "(ceil(window / 16) + 1 pages per sequence) instead of full page tables")
@@ -162,6 +165,13 @@ def cpu_baseline(w, copy0, budget_s):
 
 # ----------------------------------------------------------------------------- main
 
+def tileable(cfg) -> bool:
+    """Whether a layer's projection weights have a tiled layout (every input
+    width a multiple of 64)."""
+    f = cfg.moe_ffn if cfg.n_experts else cfg.ffn
+    return cfg.hidden % 64 == 0 and (cfg.n_q * cfg.head_dim) % 64 == 0 and f % 64 == 0
+
+
 def ffn_sweep(args):
     """Dense FFN stage ([6,10) of the 8B-shaped layer) at growing batch: the
     weights stream once per call, so the GEMMs are HBM-bound at small batch and
@@ -187,7 +197,7 @@ def ffn_sweep(args):
         for c in range(copies):
             wts = [gen.layer_weights(cfg, base.seed + 1000 * c, 0, dev, base.router_std)]
             pools = [gen.kv_pool(cfg, M, base.seed + 1000 * c, 0, dev)]
-            blk = R.DeviceBlock([cfg], wts, pools, M)
+            blk = R.DeviceBlock([cfg], wts, pools, M, tiled=args.weights == "tiled")
             st = R.DeviceState(blk, batch, dev)
             st.view("resid", M, cfg.hidden).copy_(gen.activations(M, cfg.hidden, base.seed + c, dev))
             sets.append((blk, st, wts, pools))
@@ -218,6 +228,7 @@ def ffn_sweep(args):
         torch.cuda.empty_cache()
     print(json.dumps({"metric": "dense FFN stage time vs batch (8B-shaped layer)", "unit": "us",
                       "steps": args.steps, "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
+                      "weight_layout": args.weights,
                       "ffn_sweep": rows}), flush=True)
 
 
@@ -240,6 +251,9 @@ def latency_table(args):
     torch.cuda.set_device(0)
     templates = [("attention stage", 0, 6), ("FFN stage", 6, 10), ("core attention", 3, 5), ("colocated layer", 0, 10)]
     weights = [gen.layer_weights(cfg, base.seed, 0, dev, base.router_std)]
+    tiled = args.weights == "tiled"
+    if tiled:
+        weights = [R.tile_weights(cfg, weights[0])]
     stream = torch.cuda.current_stream().cuda_stream
 
     def median_us(fn):
@@ -265,7 +279,7 @@ def latency_table(args):
             assert B.ods_kv_alloc(P, ctx, M, base.seed, max_pages, table) == 0, B.ods_last_error()
             batch = R.DeviceBatch(torch.from_numpy(ctx).to(dev), torch.from_numpy(table).to(dev))
             pools = [gen.kv_pool(cfg, P, base.seed, 0, dev)]
-            blk = R.DeviceBlock([cfg], weights, pools, P)
+            blk = R.DeviceBlock([cfg], weights, pools, P, pretiled=tiled)
             st = R.DeviceState(blk, batch, dev)
             x = gen.activations(M, cfg.hidden, base.seed, dev)
             for i in range(10):  # single operators, eager, for per-operator latency models
@@ -290,7 +304,8 @@ def latency_table(args):
             torch.cuda.empty_cache()
     print(json.dumps({"metric": "stage latency t_j = f_lat(op range, batch, context), dense 8B-shaped layer",
                       "unit": "us", "steps": args.steps, "warmup": args.warmup, "dtype": "bf16",
-                      "data": "synthetic", "latency_table": rows, "op_latency": op_rows}), flush=True)
+                      "data": "synthetic", "weight_layout": args.weights, "latency_table": rows,
+                      "op_latency": op_rows}), flush=True)
 
 
 def main():
@@ -336,6 +351,7 @@ def main():
         ring_table = np.zeros((w.batch, ring_pages), dtype=np.int32)
         assert B.ods_kv_alloc(P_ring, rctx, w.batch, w.seed + 7, ring_pages, ring_table) == 0, B.ods_last_error()
     layer_pages = [P_ring if (ring_pages and c.window > 0) else P for c in w.layers]
+    tiled = args.weights == "tiled" and all(tileable(c) for c in w.layers)
     kv_pool_bytes = [B.ods_kv_pool_bytes(R.layer_cfg(c), n) for c, n in zip(w.layers, layer_pages)]
 
     batch = R.DeviceBatch(torch.from_numpy(ctx).to(dev), torch.from_numpy(page_table).to(dev),
@@ -347,7 +363,7 @@ def main():
                    for l, cfg in enumerate(w.layers)]
         pools = [gen.kv_pool(cfg, n, seed, l, dev) for l, (cfg, n) in enumerate(zip(w.layers, layer_pages))]
         x = gen.activations(w.batch, w.layers[0].hidden, seed, dev)
-        blk = R.DeviceBlock(w.layers, weights, pools, layer_pages)
+        blk = R.DeviceBlock(w.layers, weights, pools, layer_pages, tiled=tiled)
         state = R.DeviceState(blk, batch, dev)
         sets.append(dict(block=blk, state=state, weights=weights, pools=pools, x=x, ctx=ctx,
                          page_table=page_table))
@@ -457,6 +473,7 @@ def main():
                    "ctx_range": [w.ctx_lo, w.ctx_hi], "ctx_mean": float(ctx.mean()),
                    "layers": n_layers, "copies_rotated": copies,
                    "step": "attention stage [0,6) then FFN stage [6,N) per layer",
+                   "weight_layout": "tiled" if tiled else "rows",
                    "kv_ring_pages": ring_pages, "kv_pool_bytes_per_layer": kv_pool_bytes,
                    "kv_pool_bytes_total": int(sum(kv_pool_bytes))},
         "stages": {"attn": stage(t_attn, attn_bytes, attn_flops), "ffn": stage(t_ffn, ffn_bytes, ffn_flops)},

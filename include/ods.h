@@ -89,7 +89,17 @@ typedef struct {
   float rope_theta, rms_eps;
 } ods_layer_cfg;
 
-/* One layer's device-resident weights (bf16, row-major "out x in") and KV pool.
+/* Layout of a layer's projection weights (w_qkv, w_o, w_gate_up, w_down).
+ *   ODS_WEIGHTS_ROWS:  row-major "out x in", as listed under ods_layer.
+ *   ODS_WEIGHTS_TILED: the tile order ods_tile_weight() writes, which the
+ *     weight-streaming GEMM reads as one contiguous run per block (faster at
+ *     decode batches). Needs hidden, n_q * head_dim and ffn (dense) or moe_ffn
+ *     (MoE) to be multiples of 64 (ODS_EUNSUPPORTED otherwise). w_router stays
+ *     row-major. */
+typedef enum { ODS_WEIGHTS_ROWS = 0, ODS_WEIGHTS_TILED = 1 } ods_weight_layout;
+
+/* One layer's device-resident weights (bf16, row-major "out x in" unless
+ * weight_layout says otherwise) and KV pool.
  *   g_attn, g_ffn  [hidden]
  *   w_qkv          [(n_q + 2 n_kv) head_dim, hidden]   q heads, then k heads, then v heads
  *   w_o            [hidden, n_q head_dim]
@@ -106,6 +116,7 @@ typedef struct {
   const void *g_attn, *w_qkv, *w_o, *g_ffn, *w_gate_up, *w_down, *w_router;
   void *kv_pool;
   int64_t pool_pages;
+  int32_t weight_layout;  /* ods_weight_layout */
 } ods_layer;
 
 /* A partition block: n_layers layers whose operators are numbered consecutively.
@@ -198,6 +209,30 @@ size_t ods_workspace_bytes(const ods_block *blk, const ods_batch *batch);
 
 /* Number of operators of the block (sum over layers of 10 or 14); < 0 on error. */
 int32_t ods_block_num_ops(const ods_block *blk);
+
+/* Tiled weight layout (ODS_WEIGHTS_TILED). A weight of `groups` slabs (1, or
+ * n_experts for the expert weights), each `out` x `in` row-major bf16 (gated:
+ * 2 out rows, the gate rows then the up rows, as w_gate_up), is stored as
+ * consecutive 16 KB tiles, slab by slab: for each N tile nt and each 64-wide
+ * K step s, 128 rows of 64 columns, row r at byte r * 128 of the tile and the
+ * row's 16-byte chunk c (columns 64 s + 8 c .. + 7) at position c ^ (r % 8)
+ * of that row. Plain weights: tile row r is weight row 128 nt + r. Gated: tile
+ * rows r < 64 are gate rows 64 nt + r, rows 64 + j the matching up rows
+ * out + 64 nt + j, so both halves of an output column stream together (the
+ * SwiGLU epilogue of the fused gate_up GEMM, Section 2's FFN operator). Rows
+ * past `out` are zero. The XOR position of the chunks keeps the GEMM's LDS
+ * fragment reads free of bank conflicts.
+ *
+ * ods_tiled_weight_bytes: bytes of that layout; 0 unless out >= 1, in >= 64,
+ *   in % 64 == 0, groups >= 1 and gated in {0, 1}.
+ * ods_tile_weight: enqueues on `stream` the conversion of the row-major weight
+ *   at src (device, groups * (gated ? 2 : 1) * out * in bf16) into dst (device,
+ *   ods_tiled_weight_bytes() bytes, not overlapping src). Both 16-byte aligned.
+ *   ODS_EINVAL for null or misaligned pointers or sizes the layout rejects;
+ *   ODS_EHIP if the launch fails. Nothing is enqueued on error. */
+size_t ods_tiled_weight_bytes(int32_t out, int32_t in, int32_t gated, int32_t groups);
+ods_status ods_tile_weight(const void *src, void *dst, int32_t out, int32_t in, int32_t gated, int32_t groups,
+                           hipStream_t stream);
 
 /* Static name of global operator `op` ("attn_core", ...), NULL if out of range. */
 const char *ods_op_name(const ods_block *blk, int32_t op);

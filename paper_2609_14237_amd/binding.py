@@ -16,6 +16,7 @@ ODS_OK, ODS_EINVAL, ODS_ERANGE, ODS_ENOMEM, ODS_EUNSUPPORTED, ODS_EHIP = 0, -1, 
 STATUS_NAMES = {0: "ODS_OK", -1: "ODS_EINVAL", -2: "ODS_ERANGE", -3: "ODS_ENOMEM",
                 -4: "ODS_EUNSUPPORTED", -5: "ODS_EHIP"}
 PAGE_TOKENS = 16
+ODS_WEIGHTS_ROWS, ODS_WEIGHTS_TILED = 0, 1
 
 BUFFERS = ("resid", "xn", "qkv", "o", "hn", "gu", "act", "logits", "topk_w", "topk_ids", "perm",
            "slot_pos", "expert_off", "xp", "gu_p", "act_p", "yp")
@@ -31,7 +32,7 @@ class ods_layer(C.Structure):
     _fields_ = [("cfg", ods_layer_cfg),
                 ("g_attn", C.c_void_p), ("w_qkv", C.c_void_p), ("w_o", C.c_void_p), ("g_ffn", C.c_void_p),
                 ("w_gate_up", C.c_void_p), ("w_down", C.c_void_p), ("w_router", C.c_void_p),
-                ("kv_pool", C.c_void_p), ("pool_pages", C.c_int64)]
+                ("kv_pool", C.c_void_p), ("pool_pages", C.c_int64), ("weight_layout", C.c_int32)]
 
 
 class ods_block(C.Structure):
@@ -74,6 +75,9 @@ SIGNATURES = {
     "ods_graph_launch": (C.c_int, [C.c_void_p, C.c_void_p]),
     "ods_graph_destroy": (C.c_int, [C.c_void_p]),
     "ods_last_error": (C.c_char_p, []),
+    "ods_tiled_weight_bytes": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32, C.c_int32]),
+    "ods_tile_weight": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                  C.c_void_p]),
 }
 
 
@@ -164,3 +168,11 @@ def ods_graph_launch(exec_handle: int, stream: int) -> int:
 
 def ods_graph_destroy(exec_handle) -> int:
     return lib.ods_graph_destroy(exec_handle)
+
+
+def ods_tiled_weight_bytes(out: int, in_: int, gated: int, groups: int) -> int:
+    return lib.ods_tiled_weight_bytes(out, in_, gated, groups)
+
+
+def ods_tile_weight(src: int, dst: int, out: int, in_: int, gated: int, groups: int, stream: int) -> int:
+    return lib.ods_tile_weight(src, dst, out, in_, gated, groups, stream)

@@ -454,6 +454,7 @@ template <int EPI>
 hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
   const int bn = tile_n(a.N, a.K, EPI);
   const int n_tiles = (a.N + bn - 1) / bn;
+  if (a.b_tiled) return launch_gemm_stream(a, s);  // tiled weights: K % 64 == 0 by contract
   if (a.group_off) {
     // Expert row groups average B*k/E rows (64 at the MoE workload). The
     // streaming kernel takes them when K is a whole number of 64-wide steps
@@ -496,8 +497,8 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
 
 }  // namespace
 
-int gemm_splits(int M, int N, int K, int epi) {
-  if (gemm_use_stream(M, N, K, epi)) return gemm_stream_splits(M, N, K, epi);
+int gemm_splits(int M, int N, int K, int epi, bool b_tiled) {
+  if (b_tiled || gemm_use_stream(M, N, K, epi)) return gemm_stream_splits(M, N, K, epi);
   if (N % 4 != 0) return 1;  // the reduce works on 4-column groups
   if (use_big(M, N)) {
     // Large-M tiles: one 512-thread block per compute unit; split K (up to 8
@@ -525,8 +526,8 @@ int gemm_splits(int M, int N, int K, int epi) {
   return s;
 }
 
-size_t gemm_partial_bytes(int M, int N, int K, int epi) {
-  const int s = gemm_splits(M, N, K, epi);
+size_t gemm_partial_bytes(int M, int N, int K, int epi, bool b_tiled) {
+  const int s = gemm_splits(M, N, K, epi, b_tiled);
   if (s <= 1) return 0;
   return (size_t)s * M * N * (epi == EPI_SILU ? 2 : 1) * sizeof(float);
 }

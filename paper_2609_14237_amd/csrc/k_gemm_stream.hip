@@ -1,10 +1,13 @@
 // Weight-streaming bf16 MFMA GEMM for M > 128 rows (the 256-row decode batch,
 // the 512-row MoE attention projections, larger prefill-sized batches), for
 // 33 to 64 rows outside the SiLU-gated FFN GEMM, and for the grouped expert
-// GEMMs (any rows per group): C[m, n] = sum_k A[m, k] * B[n, k] with the same
-// epilogues as the other GEMM kernels. Built on its own with MFMA results in
+// GEMMs (any rows per group), and for every GEMM on tiled weights (B stored
+// as the LDS image of each K step's tile, read as one contiguous run per
+// block): C[m, n] = sum_k A[m, k] * B[n, k] with the same epilogues as the
+// other GEMM kernels. Built on its own with MFMA results in
 // VGPRs (the build passes -amdgpu-mfma-vgpr-form for this file only), which
 // keeps the accumulators in place across the K loop.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.hpp"
@@ -101,13 +104,21 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
   // chunk c = (lane % 8) ^ (row % 8) of that row, so chunk c of row r sits at
   // position c ^ (r % 8).
   const int chunk = ((lane & 7) ^ (lane >> 3)) * 8;
+  // Tiled weights hold each step's tile as its LDS image, so load q of a wave
+  // copies 1 KB of it verbatim: the block streams one contiguous run of its
+  // N tile's K range instead of 128 separate rows.
   const uint16_t *bptr[BL];
+  const int64_t bstep = p.b_tiled ? BNR * BK : BK;  // elements between consecutive K steps of a load
 #pragma unroll
   for (int q = 0; q < BL; ++q) {
-    const int r = (wave * BL + q) * 8 + (lane >> 3);
-    const int n = min(n0 + (SILU ? r % BN : r), p.N - 1);
-    const int row = SILU && r >= BN ? p.n_up + n : n;
-    bptr[q] = Bg + (int64_t)row * p.ldb + (int64_t)s_begin * BK + chunk;
+    if (p.b_tiled) {
+      bptr[q] = Bg + ((int64_t)nt * steps + s_begin) * (BNR * BK) + (wave * BL + q) * 512 + lane * 8;
+    } else {
+      const int r = (wave * BL + q) * 8 + (lane >> 3);
+      const int n = min(n0 + (SILU ? r % BN : r), p.N - 1);
+      const int row = SILU && r >= BN ? p.n_up + n : n;
+      bptr[q] = Bg + (int64_t)row * p.ldb + (int64_t)s_begin * BK + chunk;
+    }
   }
   // Fragment read: row 16i + lane % 16, chunk 4 ks + lane / 16. B tile row of
   // fragment jt: SiLU takes gate rows (64 / WN) wn + 16 jt (jt < TN / 2) and the
@@ -157,7 +168,7 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
 #pragma unroll
         for (int q = 0; q < BL; ++q)
           __builtin_amdgcn_global_load_lds(
-              (const void *)(bptr[q] + k),
+              (const void *)(bptr[q] + min(t, last) * bstep),
               (__attribute__((address_space(3))) void *)(lds_b + slot * BSTAGE + (wave * BL + q) * 1024), 16, 0, 0);
       };
       auto read_frags = [&](Frags &f, int slot) {
@@ -241,13 +252,23 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
     if (!live) continue;
 
     // Epilogue: lane holds rows (lane >> 4) * 4 + e of column lane & 15 of each 16x16 tile.
+    // A plain epilogue over gated tiles maps tile row rr to gate column
+    // 64 nt + rr (rr < 64) or up column n_up + 64 nt + rr - 64.
     constexpr int TO = SILU ? TN / 2 : TN;  // output fragments (SiLU pairs gate jt with up jt + TO)
+    const bool gated_cols = !SILU && p.b_tiled && p.n_up > 0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
       for (int jt = 0; jt < TO; ++jt) {
-        const int n = n0 + (SILU ? wn * (64 / WN) : wn * (128 / WN)) + jt * 16 + (lane & 15);
-        if (n >= p.N) continue;
+        const int rr = (SILU ? wn * (64 / WN) : wn * (128 / WN)) + jt * 16 + (lane & 15);
+        int n = n0 + rr;
+        if (gated_cols) {
+          const int c = nt * 64 + (rr & 63);
+          if (c >= p.n_up) continue;
+          n = rr < 64 ? c : p.n_up + c;
+        } else if (n >= p.N) {
+          continue;
+        }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + e;
@@ -314,7 +335,48 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
   return launch_splitk_reduce(a, s);
 }
 
+// One thread per 16-byte chunk of the tiled weight (the order tile_weight
+// documents); rows past `out` are written as zeros.
+__global__ __launch_bounds__(256) void tile_weight_kernel(const uint16_t *__restrict__ src,
+                                                          uint16_t *__restrict__ dst, int out, int in, int gated,
+                                                          int n_tiles, int64_t n_chunks) {
+  const int ks = in / 64;
+  const int64_t src_rows = gated ? 2 * (int64_t)out : out;
+  for (int64_t c = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; c < n_chunks;
+       c += (int64_t)gridDim.x * blockDim.x) {
+    const int pos = (int)(c & 7);
+    const int r = (int)((c >> 3) & 127);
+    const int64_t tile = c >> 10;  // (slab * n_tiles + nt) * ks + s
+    const int s = (int)(tile % ks);
+    const int64_t st = tile / ks;
+    const int nt = (int)(st % n_tiles);
+    const int64_t slab = st / n_tiles;
+    const int n = gated ? nt * 64 + (r & 63) : nt * 128 + r;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (n < out) {
+      const int64_t row = slab * src_rows + (gated && r >= 64 ? out + n : n);
+      v = *(const u32x4 *)(src + row * in + s * 64 + ((pos ^ (r & 7)) << 3));
+    }
+    *(u32x4 *)(dst + c * 8) = v;
+  }
+}
+
 }  // namespace
+
+int64_t tiled_weight_elems(int out, int in, bool gated, int groups) {
+  const int64_t tiles = gated ? (out + 63) / 64 : (out + 127) / 128;
+  return (int64_t)groups * tiles * (in / 64) * (128 * 64);
+}
+
+hipError_t launch_tile_weight(const uint16_t *src, uint16_t *dst, int out, int in, bool gated, int groups,
+                              hipStream_t s) {
+  const int n_tiles = gated ? (out + 63) / 64 : (out + 127) / 128;
+  const int64_t n_chunks = tiled_weight_elems(out, in, gated, groups) / 8;
+  const int64_t blocks = std::min<int64_t>((n_chunks + 255) / 256, 65536);
+  hipLaunchKernelGGL(tile_weight_kernel, dim3((unsigned)blocks), dim3(256), 0, s, src, dst, out, in, gated ? 1 : 0,
+                     n_tiles, n_chunks);
+  return hipGetLastError();
+}
 
 // Dense GEMMs past 128 rows, and those of 33 to 64 rows except the SiLU-gated
 // one (64-row tiles: at 64 rows qkv 20.2 -> 18.0 us, o_proj 16.4 -> 15.9 us and

@@ -25,18 +25,31 @@ struct GemmArgs {
   int splits;                 // split-K count (>1: fp32 partials in `partial`, then a reduce)
   float *partial;
   int defer_reduce;           // splits > 1: leave the partials for a consumer that sums them itself
+  int b_tiled;                // B in the streaming kernel's tile order (tile_weight); with n_up > 0
+                              // the tiles pair gate and up rows, whatever the epilogue
 };
+
+// Tile order of a weight for the streaming GEMM: for each group, N tile and
+// 64-wide K step, the 16 KB image of that step's 128 B rows in LDS (row r at
+// r * 128 bytes, 16-byte chunk c of the row at position c ^ (r % 8)). Plain
+// weights put rows 128 nt .. +127 in N tile nt; gated (gate rows, then up
+// rows, `out` of each) put gate rows 64 nt .. +63 then the matching up rows.
+// Rows past `out` are zero. `in` must be a multiple of 64.
+int64_t tiled_weight_elems(int out, int in, bool gated, int groups);
+hipError_t launch_tile_weight(const uint16_t *src, uint16_t *dst, int out, int in, bool gated, int groups,
+                              hipStream_t s);
 
 // Compute units of the current device (queried once per process and device).
 int num_cus();
 
 // Split-K plan for a dense GEMM (shared by sizing and launching).
-int gemm_splits(int M, int N, int K, int epi);
-size_t gemm_partial_bytes(int M, int N, int K, int epi);
+int gemm_splits(int M, int N, int K, int epi, bool b_tiled = false);
+size_t gemm_partial_bytes(int M, int N, int K, int epi, bool b_tiled = false);
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
 // Sum of split-K partials plus the epilogue (after a partial-writing launch).
 hipError_t launch_splitk_reduce(const GemmArgs &a, hipStream_t s);
-// Weight-streaming kernel for dense GEMMs past 128 rows (K % 64 == 0).
+// Weight-streaming kernel (K % 64 == 0): dense GEMMs past 128 rows, of 33 to
+// 64 rows but the SiLU-gated one, grouped GEMMs, and every GEMM on tiled weights.
 bool gemm_use_stream(int M, int N, int K, int epi);
 int gemm_stream_splits(int M, int N, int K, int epi);
 hipError_t launch_gemm_stream(const GemmArgs &a, hipStream_t s);

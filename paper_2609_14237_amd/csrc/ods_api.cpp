@@ -74,11 +74,23 @@ ods_status check_cfg(const ods_layer_cfg &c, int layer) {
   return ODS_OK;
 }
 
+bool tiled(const ods_layer &L) { return L.weight_layout == ODS_WEIGHTS_TILED; }
+
 ods_status check_block(const ods_block *blk) {
   if (!blk || !blk->layers || blk->n_layers <= 0) return fail(ODS_EINVAL, "null or empty block");
   for (int l = 0; l < blk->n_layers; ++l) {
-    ods_status st = check_cfg(blk->layers[l].cfg, l);
+    const ods_layer &L = blk->layers[l];
+    ods_status st = check_cfg(L.cfg, l);
     if (st != ODS_OK) return st;
+    if (L.weight_layout != ODS_WEIGHTS_ROWS && L.weight_layout != ODS_WEIGHTS_TILED)
+      return fail(ODS_EINVAL, "layer %d: weight_layout %d", l, L.weight_layout);
+    if (tiled(L)) {
+      const ods_layer_cfg &c = L.cfg;
+      const int f = is_moe(c) ? c.moe_ffn : c.ffn;
+      if (c.hidden % 64 != 0 || (c.n_q * c.head_dim) % 64 != 0 || f % 64 != 0)
+        return fail(ODS_EUNSUPPORTED, "layer %d: tiled weights need hidden, n_q * head_dim and the FFN width "
+                    "to be multiples of 64", l);
+    }
   }
   return ODS_OK;
 }
@@ -124,18 +136,20 @@ AttnPlan plan_for(const ods_layer_cfg &c, const ods_batch *b) {
   return attn_plan(b->batch, c.n_kv, c.head_dim, kv_map(c, b).cols, c.window, b->split_pages);
 }
 
-size_t layer_ws_bytes(const ods_layer_cfg &c, const ods_batch *b) {
+size_t layer_ws_bytes(const ods_layer &L, const ods_batch *b) {
+  const ods_layer_cfg &c = L.cfg;
   const int B = b->batch;
+  const bool t = tiled(L);
   size_t w = align_up(attn_ws_bytes(B, c.n_q, c.n_kv, c.head_dim, plan_for(c, b)));
-  auto g = [&](int N, int K, int epi) { w = std::max(w, align_up(gemm_partial_bytes(B, N, K, epi))); };
-  g(qkv_dim(c), c.hidden, EPI_BF16);
-  g(c.hidden, c.n_q * c.head_dim, EPI_RESID);
+  auto g = [&](int N, int K, int epi, bool bt) { w = std::max(w, align_up(gemm_partial_bytes(B, N, K, epi, bt))); };
+  g(qkv_dim(c), c.hidden, EPI_BF16, t);
+  g(c.hidden, c.n_q * c.head_dim, EPI_RESID, t);
   if (is_moe(c)) {
-    g(c.n_experts, c.hidden, EPI_F32);
+    g(c.n_experts, c.hidden, EPI_F32, false);  // the router stays row-major
   } else {
-    g(c.ffn, c.hidden, EPI_SILU);
-    g(2 * c.ffn, c.hidden, EPI_BF16);
-    g(c.hidden, c.ffn, EPI_RESID);
+    g(c.ffn, c.hidden, EPI_SILU, t);
+    g(2 * c.ffn, c.hidden, EPI_BF16, t);
+    g(c.hidden, c.ffn, EPI_RESID, t);
   }
   return w;
 }
@@ -230,7 +244,7 @@ size_t ods_live_bytes(const ods_block *blk, int32_t batch, ods_buffer which) {
 size_t ods_workspace_bytes(const ods_block *blk, const ods_batch *batch) {
   if (check_block(blk) != ODS_OK || !batch || batch->batch < 0 || batch->max_pages <= 0) return 0;
   size_t w = 256;
-  for (int l = 0; l < blk->n_layers; ++l) w = std::max(w, layer_ws_bytes(blk->layers[l].cfg, batch));
+  for (int l = 0; l < blk->n_layers; ++l) w = std::max(w, layer_ws_bytes(blk->layers[l], batch));
   return w;
 }
 
@@ -337,7 +351,7 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
     if (is_moe(c) && (int64_t)B * c.top_k > INT32_MAX / 2) return fail(ODS_ERANGE, "batch * top_k too large");
   }
   size_t ws_need = 0;
-  for (auto &o : ops) ws_need = std::max(ws_need, layer_ws_bytes(blk->layers[o.layer].cfg, batch));
+  for (auto &o : ops) ws_need = std::max(ws_need, layer_ws_bytes(blk->layers[o.layer], batch));
   bool uses_ws = false;
   for (auto &o : ops)
     if (o.kind == K_ATTN_CORE || o.kind == K_QKV || o.kind == K_O_PROJ || o.kind == K_GATE_UP ||
@@ -365,14 +379,16 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
     hipError_t e = hipSuccess;
     const char *what = kNames[k];
     GemmArgs ga{};
+    const bool wt = tiled(L);  // projection weights in tile order (the router never is)
     auto dense_gemm = [&](const void *A, const void *Bw, void *C, int N, int K, int epi, int n_up, int ldc,
-                          bool defer_reduce = false) {
+                          bool defer_reduce = false, bool b_tiled = false) {
       ga.A = (const uint16_t *)A; ga.lda = K;
       ga.B = (const uint16_t *)Bw; ga.ldb = K; ga.b_group_stride = 0;
       ga.C = C; ga.ldc = ldc;
       ga.M = B; ga.N = N; ga.K = K; ga.n_up = n_up; ga.epi = epi;
       ga.group_off = nullptr; ga.groups = 0;
-      ga.splits = gemm_splits(B, N, K, epi);
+      ga.b_tiled = b_tiled ? 1 : 0;
+      ga.splits = gemm_splits(B, N, K, epi, b_tiled);
       ga.partial = (float *)st->ws;
       ga.defer_reduce = defer_reduce ? 1 : 0;
       return launch_gemm(ga, stream);
@@ -383,8 +399,9 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
       case K_QKV: {
         // With split-K and RoPE next in the range, the RoPE / KV-append kernel
         // sums the partials itself (same order and rounding as the reduce).
-        const bool fuse = next_same_layer && ops[i + 1].kind == K_ROPE && gemm_splits(B, qkv_dim(c), H, EPI_BF16) > 1;
-        e = dense_gemm(st->xn, L.w_qkv, st->qkv, qkv_dim(c), H, EPI_BF16, 0, qkv_dim(c), fuse);
+        const bool fuse =
+            next_same_layer && ops[i + 1].kind == K_ROPE && gemm_splits(B, qkv_dim(c), H, EPI_BF16, wt) > 1;
+        e = dense_gemm(st->xn, L.w_qkv, st->qkv, qkv_dim(c), H, EPI_BF16, 0, qkv_dim(c), fuse, wt);
         if (fuse && e == hipSuccess) {
           const bool app = i + 2 < ops.size() && ops[i + 2].layer == ops[i].layer && ops[i + 2].kind == K_KV_APPEND;
           const KvMap m = kv_map(c, batch);
@@ -415,18 +432,19 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
                              U(L.kv_pool), L.pool_pages, plan_for(c, batch), (float *)st->ws, U(st->o), stream);
         break;
       }
-      case K_O_PROJ: e = dense_gemm(st->o, L.w_o, st->resid, H, c.n_q * D, EPI_RESID, 0, H); break;
+      case K_O_PROJ: e = dense_gemm(st->o, L.w_o, st->resid, H, c.n_q * D, EPI_RESID, 0, H, false, wt); break;
       case K_GATE_UP:
         if (next_same_layer && ops[i + 1].kind == K_SILU) {
-          e = dense_gemm(st->hn, L.w_gate_up, st->act, c.ffn, H, EPI_SILU, c.ffn, c.ffn);
+          e = dense_gemm(st->hn, L.w_gate_up, st->act, c.ffn, H, EPI_SILU, c.ffn, c.ffn, false, wt);
           what = "gate_up+silu_mul";
           ++i;
         } else {
-          e = dense_gemm(st->hn, L.w_gate_up, st->gu, 2 * c.ffn, H, EPI_BF16, 0, 2 * c.ffn);
+          // tiled gate_up pairs gate and up rows per tile: n_up tells the plain epilogue where the up half goes
+          e = dense_gemm(st->hn, L.w_gate_up, st->gu, 2 * c.ffn, H, EPI_BF16, wt ? c.ffn : 0, 2 * c.ffn, false, wt);
         }
         break;
       case K_SILU: e = launch_silu_mul(U(st->gu), U(st->act), B, c.ffn, stream); break;
-      case K_DOWN: e = dense_gemm(st->act, L.w_down, st->resid, H, c.ffn, EPI_RESID, 0, H); break;
+      case K_DOWN: e = dense_gemm(st->act, L.w_down, st->resid, H, c.ffn, EPI_RESID, 0, H, false, wt); break;
       case K_ROUTER: e = dense_gemm(st->hn, L.w_router, st->logits, c.n_experts, H, EPI_F32, 0, c.n_experts); break;
       case K_TOPK: e = launch_topk(st->logits, B, c.n_experts, c.top_k, st->topk_ids, st->topk_w, stream); break;
       case K_PERMUTE:
@@ -445,19 +463,22 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
         ga.groups = c.n_experts;
         ga.splits = 1;
         ga.partial = nullptr;
+        ga.b_tiled = wt ? 1 : 0;
         if (k == K_EXP_GATE_UP) {
           ga.A = U(st->xp); ga.lda = H; ga.K = H;
-          ga.B = U(L.w_gate_up); ga.ldb = H; ga.b_group_stride = (int64_t)2 * I * H;
+          ga.B = U(L.w_gate_up); ga.ldb = H;
+          ga.b_group_stride = wt ? tiled_weight_elems(I, H, true, 1) : (int64_t)2 * I * H;
           if (fuse) {
             ga.C = st->act_p; ga.ldc = I; ga.N = I; ga.n_up = I; ga.epi = EPI_SILU;
             what = "expert_gate_up+silu_mul";
             ++i;
           } else {
-            ga.C = st->gu_p; ga.ldc = 2 * I; ga.N = 2 * I; ga.n_up = 0; ga.epi = EPI_BF16;
+            ga.C = st->gu_p; ga.ldc = 2 * I; ga.N = 2 * I; ga.n_up = wt ? I : 0; ga.epi = EPI_BF16;
           }
         } else {
           ga.A = U(st->act_p); ga.lda = I; ga.K = I;
-          ga.B = U(L.w_down); ga.ldb = I; ga.b_group_stride = (int64_t)H * I;
+          ga.B = U(L.w_down); ga.ldb = I;
+          ga.b_group_stride = wt ? tiled_weight_elems(H, I, false, 1) : (int64_t)H * I;
           ga.C = st->yp; ga.ldc = H; ga.N = H; ga.n_up = 0; ga.epi = EPI_BF16;
         }
         e = launch_gemm(ga, stream);
@@ -472,6 +493,26 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
     if (e != hipSuccess) return fail(ODS_EHIP, "launch of %s (layer %d) failed: %s", what, ops[i].layer,
                                      hipGetErrorString(e));
   }
+  g_err[0] = 0;
+  return ODS_OK;
+}
+
+size_t ods_tiled_weight_bytes(int32_t out, int32_t in, int32_t gated, int32_t groups) {
+  if (out < 1 || in < 64 || in % 64 != 0 || groups < 1 || (gated != 0 && gated != 1)) return 0;
+  return (size_t)tiled_weight_elems(out, in, gated != 0, groups) * 2;
+}
+
+ods_status ods_tile_weight(const void *src, void *dst, int32_t out, int32_t in, int32_t gated, int32_t groups,
+                           hipStream_t stream) {
+  const size_t bytes = ods_tiled_weight_bytes(out, in, gated, groups);
+  if (!bytes) return fail(ODS_EINVAL, "ods_tile_weight: out %d, in %d, gated %d, groups %d", out, in, gated, groups);
+  if (!src || !dst) return fail(ODS_EINVAL, "ods_tile_weight: null pointer");
+  if (!aligned16(src) || !aligned16(dst)) return fail(ODS_EINVAL, "ods_tile_weight: pointers must be 16-byte aligned");
+  const size_t src_bytes = (size_t)groups * (gated ? 2 : 1) * out * in * 2;
+  const uintptr_t s0 = (uintptr_t)src, d0 = (uintptr_t)dst;
+  if (s0 < d0 + bytes && d0 < s0 + src_bytes) return fail(ODS_EINVAL, "ods_tile_weight: src and dst overlap");
+  const hipError_t e = launch_tile_weight((const uint16_t *)src, (uint16_t *)dst, out, in, gated != 0, groups, stream);
+  if (e != hipSuccess) return fail(ODS_EHIP, "ods_tile_weight: %s", hipGetErrorString(e));
   g_err[0] = 0;
   return ODS_OK;
 }

@@ -23,13 +23,47 @@ def _ptr(t):
     return t.data_ptr()
 
 
+def _tile_shapes(cfg):
+    """(out, in, gated, groups) of each projection weight, as ods_tile_weight takes them."""
+    qkv = (cfg.n_q + 2 * cfg.n_kv) * cfg.head_dim
+    H, E = cfg.hidden, cfg.n_experts
+    shapes = {"w_qkv": (qkv, H, 0, 1), "w_o": (H, cfg.n_q * cfg.head_dim, 0, 1)}
+    if E:
+        shapes.update(w_gate_up=(cfg.moe_ffn, H, 1, E), w_down=(H, cfg.moe_ffn, 0, E))
+    else:
+        shapes.update(w_gate_up=(cfg.ffn, H, 1, 1), w_down=(H, cfg.ffn, 0, 1))
+    return shapes
+
+
+def tile_weights(cfg, w: dict, stream=None) -> dict:
+    """Tiled copies (ODS_WEIGHTS_TILED) of a layer's projection weights, converted
+    by ods_tile_weight on the device; the other entries of w are passed through."""
+    stream = stream if stream is not None else torch.cuda.current_stream()
+    out = dict(w)
+    for name, (o, i, gated, groups) in _tile_shapes(cfg).items():
+        src = w[name]
+        n = _b.ods_tiled_weight_bytes(o, i, gated, groups)
+        if n == 0:
+            raise ValueError(f"{name}: no tiled layout for out={o}, in={i} (in must be a multiple of 64)")
+        dst = torch.empty(n // 2, dtype=torch.bfloat16, device=src.device)
+        _b._check(_b.ods_tile_weight(src.data_ptr(), dst.data_ptr(), o, i, gated, groups, stream.cuda_stream),
+                  f"ods_tile_weight({name})")
+        out[name] = dst
+    return out
+
+
 class DeviceBlock:
     """ods_block over per-layer weight dicts and KV pools (tensors stay referenced).
-    pool_pages is one count for every layer or a list with one per layer."""
+    pool_pages is one count for every layer or a list with one per layer. With
+    tiled=True the projection weights are converted once into the tiled layout
+    (ODS_WEIGHTS_TILED) the weight-streaming GEMM reads fastest, and the block
+    references those copies; pretiled=True takes weights tile_weights() already
+    converted."""
 
-    def __init__(self, cfgs, weights, pools, pool_pages):
+    def __init__(self, cfgs, weights, pools, pool_pages, tiled: bool = False, pretiled: bool = False):
         self.cfgs = list(cfgs)
-        self.weights = list(weights)
+        self.tiled = tiled or pretiled
+        self.weights = [tile_weights(c, w) if tiled and not pretiled else w for c, w in zip(self.cfgs, weights)]
         self.pools = list(pools)
         n = len(self.cfgs)
         pages = list(pool_pages) if isinstance(pool_pages, (list, tuple)) else [pool_pages] * n
@@ -41,6 +75,7 @@ class DeviceBlock:
                 setattr(L, name, _ptr(w.get(name)))
             L.kv_pool = _ptr(pool)
             L.pool_pages = pages[i] if pool is not None else 0
+            L.weight_layout = _b.ODS_WEIGHTS_TILED if self.tiled else _b.ODS_WEIGHTS_ROWS
         self.c = ods_block(n, C.cast(self._layers, C.POINTER(ods_layer)))
 
     def num_ops(self) -> int:

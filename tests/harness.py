@@ -37,7 +37,7 @@ class Setup:
     """One workload instantiated on the device (and optionally mirrored for the oracle)."""
 
     def __init__(self, w: W.Workload, seed: int = 0, device="cuda", split_pages: int = 0,
-                 gen_device: str | None = None, ctx=None, alloc_seed=None, nan_trap=False):
+                 gen_device: str | None = None, ctx=None, alloc_seed=None, nan_trap=False, tiled=False):
         from paper_2609_14237_amd import binding as B
         from paper_2609_14237_amd import runtime as R
         self.w = w
@@ -58,7 +58,8 @@ class Setup:
             for l, cfg in enumerate(w.layers):
                 self._plant_nans(self.pools[l], cfg)
         self.x = gen.activations(w.batch, w.layers[0].hidden, seed, gdev).to(device)
-        self.block = R.DeviceBlock(w.layers, self.weights, self.pools, self.pool_pages)
+        # the block may hold tiled copies of the projection weights; self.weights stays row-major
+        self.block = R.DeviceBlock(w.layers, self.weights, self.pools, self.pool_pages, tiled=tiled)
         self.batch = R.DeviceBatch(torch.from_numpy(self.ctx).to(device),
                                    torch.from_numpy(self.page_table).to(device), split_pages)
         self.state = R.DeviceState(self.block, self.batch, device, fill=float("nan"))

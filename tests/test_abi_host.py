@@ -189,3 +189,43 @@ def test_ring_pages_validation():
     full = fake_block([W.TINY.layers[0]])
     batch = B.ods_batch(4, 8, FAKE, FAKE, 0, 1, None)
     assert B.ods_workspace_bytes(full.c, batch) > 0
+
+
+def test_tiled_weight_sizes_and_errors():
+    """16 KB per (slab, N tile, 64-wide K step); N tiles of 128 rows, or 64 gate
+    plus 64 up rows for a gated weight, with the last tile zero-padded."""
+    KB16 = 16 * 1024
+    assert B.ods_tiled_weight_bytes(4096, 4096, 0, 1) == 32 * 64 * KB16
+    assert B.ods_tiled_weight_bytes(14336, 4096, 1, 1) == 224 * 64 * KB16
+    assert B.ods_tiled_weight_bytes(1536, 4096, 1, 64) == 64 * 24 * 64 * KB16
+    assert B.ods_tiled_weight_bytes(130, 128, 0, 3) == 3 * 2 * 2 * KB16
+    assert B.ods_tiled_weight_bytes(65, 64, 1, 1) == 2 * 1 * KB16
+    far = FAKE + (1 << 32)
+    for args in [(0, 64, 0, 1), (64, 96, 0, 1), (64, 0, 0, 1), (64, 64, 2, 1), (64, 64, 0, 0)]:
+        assert B.ods_tiled_weight_bytes(*args) == 0, args
+        assert B.ods_tile_weight(FAKE, far, *args, 0) == B.ODS_EINVAL, args
+    assert B.ods_tile_weight(None, far, 64, 64, 0, 1, 0) == B.ODS_EINVAL
+    assert B.ods_tile_weight(FAKE + 2, far, 64, 64, 0, 1, 0) == B.ODS_EINVAL
+    assert "aligned" in B.ods_last_error()
+    assert B.ods_tile_weight(FAKE, FAKE + 4096, 64, 64, 0, 1, 0) == B.ODS_EINVAL  # dst overlaps src
+    assert "overlap" in B.ods_last_error()
+
+
+def test_tiled_layout_validation():
+    """Tiled weights need every projection's input width to be a multiple of 64;
+    an unknown layout value is rejected."""
+    tiny = fake_block(W.TINY.layers)  # ffn 688 = 10.75 x 64
+    tiny._layers[0].weight_layout = B.ODS_WEIGHTS_TILED
+    assert B.ods_run_partition(tiny.c, 0, 1, fake_batch(), fake_state(), 0) == B.ODS_EUNSUPPORTED
+    assert "multiples of 64" in B.ods_last_error()
+    assert B.ods_workspace_bytes(tiny.c, fake_batch()) == 0
+    odd = fake_block([replace(W.TINY.layers[0], ffn=704)])
+    odd._layers[0].weight_layout = 7
+    assert B.ods_run_partition(odd.c, 0, 1, fake_batch(), fake_state(), 0) == B.ODS_EINVAL
+    assert "weight_layout" in B.ods_last_error()
+    moe = fake_block([replace(W.MOE_B512.layers[0], moe_ffn=1544)])
+    moe._layers[0].weight_layout = B.ODS_WEIGHTS_TILED
+    assert B.ods_run_partition(moe.c, 0, 1, fake_batch(), fake_state(), 0) == B.ODS_EUNSUPPORTED
+    ok = fake_block(W.DENSE_8B_B64.layers)
+    ok._layers[0].weight_layout = B.ODS_WEIGHTS_TILED
+    assert B.ods_workspace_bytes(ok.c, fake_batch(64, 256)) > 0

@@ -1,0 +1,171 @@
+"""Tiled projection weights (ODS_WEIGHTS_TILED), through the C ABI.
+
+- ods_tile_weight is a pure permutation: its output equals, bit for bit, a
+  numpy rearrangement written from the layout's definition in include/ods.h.
+- A layer run on tiled weights matches the oracle (which takes the row-major
+  weights) to the same 1e-2 bar as the row-major path, at batches that take
+  the 64-row and the 256-row streaming tiles, with N tails, split-K partials
+  and the unfused gate_up (whose plain epilogue un-pairs the gate and up rows).
+- Where the row-major path runs the same streaming kernel with the same
+  split, both layouts give bit-identical results."""
+import sys
+from dataclasses import replace
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from harness import Setup, assert_close, f64, oracle_run
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2609_14237_amd import binding as B  # noqa: E402
+
+
+def say(*a):
+    print("[case]", *a, file=sys.stderr, flush=True)
+
+
+def fresh(inp):
+    out = dict(inp)
+    out["pools"] = [p.copy() for p in inp["pools"]]
+    return out
+
+
+def tiled_reference(w: np.ndarray, out: int, gated: bool) -> np.ndarray:
+    """[groups, rows, in] uint16 -> the tiled layout as a flat uint16 array:
+    per slab, N tile and 64-wide K step, 128 rows x 8 chunks of 8 columns, with
+    chunk c of row r at position c ^ (r % 8); rows past `out` are zero."""
+    groups, _, k_in = w.shape
+    per = 64 if gated else 128
+    n_tiles, ks = -(-out // per), k_in // 64
+    r = np.arange(128)
+    n = np.arange(n_tiles)[:, None] * per + (r % 64 if gated else r)[None, :]  # [nt, 128]
+    valid = n < out
+    src_row = np.where(gated & (r[None, :] >= 64), out + n, n)
+    src_row = np.where(valid, src_row, 0)
+    pos = np.arange(8)
+    chunk = pos[None, :] ^ (r[:, None] % 8)                                      # [128, 8] chunk at position
+    cols = np.arange(ks)[:, None, None, None] * 64 + chunk[None, :, :, None] * 8 + np.arange(8)  # [ks,128,8,8]
+    res = np.zeros((groups, n_tiles, ks, 128, 8, 8), dtype=np.uint16)
+    for g in range(groups):
+        rows = w[g][src_row]                                                      # [nt, 128, in]
+        # rows[nt, r, cols[s, r, p, e]] -> [nt, s, r, p, e]
+        gathered = np.take_along_axis(rows[:, None, :, :],
+                                      np.broadcast_to(cols.reshape(1, ks, 128, 64), (n_tiles, ks, 128, 64)),
+                                      axis=3).reshape(n_tiles, ks, 128, 8, 8)
+        gathered[~np.broadcast_to(valid[:, None, :, None, None], gathered.shape)] = 0
+        res[g] = gathered
+    return res.reshape(-1)
+
+
+@pytest.mark.parametrize("out,k_in,gated,groups", [(300, 192, 0, 1), (100, 128, 1, 1), (130, 64, 0, 3),
+                                                   (70, 256, 1, 2), (4096, 128, 0, 1)])
+def test_tile_weight_is_the_documented_permutation(out, k_in, gated, groups):
+    say("tile weight", out, k_in, gated, groups)
+    rows = (2 if gated else 1) * out
+    gen_ = torch.Generator().manual_seed(out * 7 + k_in)
+    src = torch.randint(-32768, 32767, (groups, rows, k_in), generator=gen_, dtype=torch.int32).to(torch.int16)
+    n = B.ods_tiled_weight_bytes(out, k_in, gated, groups)
+    dev_src = src.cuda()
+    dst = torch.full((n // 2,), -1, dtype=torch.int16, device="cuda")
+    st = B.ods_tile_weight(dev_src.data_ptr(), dst.data_ptr(), out, k_in, gated, groups,
+                           torch.cuda.current_stream().cuda_stream)
+    assert st == B.ODS_OK, B.ods_last_error()
+    torch.cuda.synchronize()
+    got = dst.cpu().numpy().view(np.uint16)
+    ref = tiled_reference(src.numpy().view(np.uint16), out, bool(gated))
+    np.testing.assert_array_equal(got, ref)
+
+
+# hidden 576 and qkv width 960 leave N tails of the 128-row tiles; ffn 704 is 11 gated tiles
+CFG = W.LayerCfg(hidden=576, n_q=9, n_kv=3, head_dim=64, ffn=704)
+
+
+def _check(s, ref, cfg, batch):
+    H = cfg.hidden
+    assert_close("resid", f64(s.buf("resid", batch, H)), ref["resid"])
+    assert_close("qkv", f64(s.buf("qkv", batch, cfg.qkv_dim)), ref["qkv"])
+    assert_close("o", f64(s.buf("o", batch, cfg.n_q * cfg.head_dim)), ref["o"])
+    assert_close("hn", f64(s.buf("hn", batch, H)), ref["hn"])
+
+
+@pytest.mark.parametrize("batch", [1, 33, 64, 100, 200])
+def test_layer_on_tiled_weights_matches_oracle(batch):
+    w = W.Workload("tiled", (CFG,), batch=batch, ctx_lo=1, ctx_hi=80)
+    say("tiled layer, batch", batch)
+    s = Setup(w, seed=31, tiled=True)
+    ref = oracle_run(fresh(s.oracle_inputs()), w.layers, 0, 10)
+    s.reset_resid()
+    s.run(0, 10)
+    torch.cuda.synchronize()
+    _check(s, ref, CFG, batch)
+    act = O.silu(ref["gu"][:, :CFG.ffn]) * ref["gu"][:, CFG.ffn:]
+    assert_close("act", f64(s.buf("act", batch, CFG.ffn)), act)
+    # unfused gate_up: gate and up columns back in their row-major places
+    s.reset_resid()
+    for a, b in [(0, 2), (2, 5), (5, 6), (6, 8), (8, 10)]:
+        s.run(a, b)
+    torch.cuda.synchronize()
+    assert_close("gu", f64(s.buf("gu", batch, 2 * CFG.ffn)), ref["gu"])
+    _check(s, ref, CFG, batch)
+
+
+@pytest.mark.parametrize("batch", [64, 200])
+def test_tiled_and_row_major_agree_bitwise_on_the_streaming_kernel(batch):
+    """qkv, o_proj and down run the streaming kernel with the same split on
+    either layout at 33-64 rows (gate_up too past 128 rows), so the outputs are
+    the same bits."""
+    w = W.Workload("tiled_vs_rows", (CFG,), batch=batch, ctx_lo=1, ctx_hi=80)
+    say("tiled vs row-major, batch", batch)
+    out = {}
+    for tiled in (False, True):
+        s = Setup(w, seed=32, tiled=tiled)
+        s.reset_resid()
+        s.run(0, 6)
+        torch.cuda.synchronize()
+        out[tiled] = {"qkv": s.buf("qkv", batch, CFG.qkv_dim).clone(), "h": s.buf("resid", batch, CFG.hidden).clone()}
+        s.run(6, 10)
+        torch.cuda.synchronize()
+        out[tiled]["y"] = s.buf("resid", batch, CFG.hidden).clone()
+    for k in ("qkv", "h") + (("y",) if batch > 128 else ()):
+        assert torch.equal(out[False][k].view(torch.int16), out[True][k].view(torch.int16)), k
+
+
+MOE_TILED = W.Workload("moe_tiled", (W.LayerCfg(hidden=512, n_q=8, n_kv=2, head_dim=64, n_experts=16, top_k=4,
+                                                moe_ffn=128),), batch=48, ctx_lo=1, ctx_hi=200,
+                       router_std=512 ** -0.5)
+
+
+@pytest.mark.parametrize("batch", [48, 300])
+def test_moe_layer_on_tiled_weights(batch):
+    """Expert slabs in tile order (64-row tiles at 12 rows per expert, 256-row
+    tiles at 75), fused and unfused expert gate_up."""
+    w = replace(MOE_TILED, batch=batch)
+    cfg = w.layers[0]
+    say("tiled moe, batch", batch)
+    s = Setup(w, seed=33, tiled=True)
+    ref = oracle_run(fresh(s.oracle_inputs()), w.layers, 0, 14)
+    # rows whose top k + 1 logits are all 3e-2 apart: the selected set and its
+    # order are then fixed beyond the ~1e-3 rounding noise of bf16 activations
+    srt = -np.sort(-ref["logits"], axis=1)[:, :cfg.top_k + 1]
+    ok = np.all(srt[:, :-1] - srt[:, 1:] > 3e-2, axis=1)
+    assert ok.mean() >= 0.4
+    for cut in ([], [11], [7, 12]):
+        say("tiled moe cut", cut)
+        s.reset_resid()
+        bounds = [0] + cut + [14]
+        for a, b in zip(bounds[:-1], bounds[1:]):
+            s.run(a, b)
+        torch.cuda.synchronize()
+        ids = s.buf("topk_ids", batch, cfg.top_k).cpu().numpy()
+        np.testing.assert_array_equal(ids[ok], ref["topk_ids"][ok])
+        rows = torch.from_numpy(np.nonzero(ok)[0]).cuda()
+        # rows whose routing is unambiguous carry the oracle's expert outputs
+        assert_close(f"resid {cut}", f64(s.buf("resid", batch, cfg.hidden).index_select(0, rows)),
+                     ref["resid"][ok])
