@@ -95,25 +95,31 @@ def _check(s, ref, cfg, batch):
     assert_close("hn", f64(s.buf("hn", batch, H)), ref["hn"])
 
 
-@pytest.mark.parametrize("batch", [1, 33, 64, 100, 200])
-def test_layer_on_tiled_weights_matches_oracle(batch):
-    w = W.Workload("tiled", (CFG,), batch=batch, ctx_lo=1, ctx_hi=80)
-    say("tiled layer, batch", batch)
+# hidden 1024 gives 16 K steps: split-K partials also for the unfused gate_up,
+# whose split epilogue writes the un-paired gate and up columns
+CFG_K16 = W.LayerCfg(hidden=1024, n_q=8, n_kv=2, head_dim=128, ffn=704)
+
+
+@pytest.mark.parametrize("cfg,batch", [(CFG, 1), (CFG, 33), (CFG, 64), (CFG, 100), (CFG, 200),
+                                       (CFG_K16, 1), (CFG_K16, 64), (CFG_K16, 150)])
+def test_layer_on_tiled_weights_matches_oracle(cfg, batch):
+    w = W.Workload("tiled", (cfg,), batch=batch, ctx_lo=1, ctx_hi=80)
+    say("tiled layer, hidden", cfg.hidden, "batch", batch)
     s = Setup(w, seed=31, tiled=True)
     ref = oracle_run(fresh(s.oracle_inputs()), w.layers, 0, 10)
     s.reset_resid()
     s.run(0, 10)
     torch.cuda.synchronize()
-    _check(s, ref, CFG, batch)
-    act = O.silu(ref["gu"][:, :CFG.ffn]) * ref["gu"][:, CFG.ffn:]
-    assert_close("act", f64(s.buf("act", batch, CFG.ffn)), act)
+    _check(s, ref, cfg, batch)
+    act = O.silu(ref["gu"][:, :cfg.ffn]) * ref["gu"][:, cfg.ffn:]
+    assert_close("act", f64(s.buf("act", batch, cfg.ffn)), act)
     # unfused gate_up: gate and up columns back in their row-major places
     s.reset_resid()
     for a, b in [(0, 2), (2, 5), (5, 6), (6, 8), (8, 10)]:
         s.run(a, b)
     torch.cuda.synchronize()
-    assert_close("gu", f64(s.buf("gu", batch, 2 * CFG.ffn)), ref["gu"])
-    _check(s, ref, CFG, batch)
+    assert_close("gu", f64(s.buf("gu", batch, 2 * cfg.ffn)), ref["gu"])
+    _check(s, ref, cfg, batch)
 
 
 @pytest.mark.parametrize("batch", [64, 200])
