@@ -335,30 +335,36 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float *__restrict
   const int b = (int)(wid / n_q), h = (int)(wid % n_q);
   const int group = n_q / n_kv;
   uint16_t *dst = o + wid * D + lane * DPL;
-  if (ctx_lens[b] < 1) {
+  // The context and the merge metadata load together (the metadata of an
+  // empty sequence is never used).
+  const int ctx = ctx_lens[b];
+  const int2 meta = ws_meta[(int64_t)b * n_kv + h / group];
+  if (ctx < 1) {
 #pragma unroll
     for (int i = 0; i < DPL; ++i) dst[i] = 0;
     return;
   }
-  const int2 meta = ws_meta[(int64_t)b * n_kv + h / group];
   const int n_seg = meta.y;
   if (n_seg <= 1) return;  // written by the attention kernel
   const int64_t rec0 = (int64_t)meta.x * group + h % group;  // records rec0 + c * group
-  float mloc = -INFINITY;
-  for (int c = lane; c < n_seg; c += 64) mloc = fmaxf(mloc, ws_ml[(rec0 + (int64_t)c * group) * 2]);
+  // (m, l) of record c as one 8-byte load; lane c keeps record c (< 64).
+  auto ml_of = [&](int c) { return *(const float2 *)(ws_ml + (rec0 + (int64_t)c * group) * 2); };
+  const float2 own = lane < n_seg ? ml_of(lane) : make_float2(-INFINITY, 0.f);
+  float mloc = own.x;
+  for (int c = lane + 64; c < n_seg; c += 64) mloc = fmaxf(mloc, ml_of(c).x);
   const float M = wave_max(mloc);
-  auto weight = [&](int c) {
-    const float mc = ws_ml[(rec0 + (int64_t)c * group) * 2];
-    return mc == -INFINITY ? 0.f : exp2f(mc - M);
-  };
-  float lsum = 0.f;
-  for (int c = lane; c < n_seg; c += 64) lsum += weight(c) * ws_ml[(rec0 + (int64_t)c * group) * 2 + 1];
+  auto weight_of = [&](float mc) { return mc == -INFINITY ? 0.f : exp2f(mc - M); };
+  float lsum = weight_of(own.x) * own.y;
+  for (int c = lane + 64; c < n_seg; c += 64) {
+    const float2 r = ml_of(c);
+    lsum += weight_of(r.x) * r.y;
+  }
   const float L = wave_sum(lsum);
   float acc[DPL];
 #pragma unroll
   for (int i = 0; i < DPL; ++i) acc[i] = 0.f;
   for (int c0 = 0; c0 < n_seg; c0 += 64) {
-    const float wl = (c0 + lane < n_seg) ? weight(c0 + lane) : 0.f;
+    const float wl = (c0 + lane < n_seg) ? (c0 == 0 ? weight_of(own.x) : weight_of(ml_of(c0 + lane).x)) : 0.f;
     const int n = min(64, n_seg - c0);
 #pragma unroll 4
     for (int j = 0; j < n; ++j) {

@@ -11,31 +11,53 @@ namespace {
 // out[r] = x[r] * (mean(x[r]^2) + eps)^(-1/2) * gain, fp32 math, bf16 out.
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t *x, const uint16_t *gain,
                                                       uint16_t *out, int H, float eps) {
+  // The row's first 4 * 256 16-byte vectors (H <= 8192) and their gains are
+  // loaded together and kept in registers; longer rows re-read the rest.
+  constexpr int VPT = 4;
   __shared__ float red[4];
   const int64_t row = blockIdx.x;
   const u32x4 *xr = (const u32x4 *)(x + row * H);
+  const u32x4 *g = (const u32x4 *)gain;
   const int nvec = H / 8;
-  float ss = 0.f;
-  for (int v = threadIdx.x; v < nvec; v += 256) {
-    const u32x4 w = xr[v];
+  u32x4 xv[VPT], gv[VPT];
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int v = threadIdx.x + i * 256;
+    if (v < nvec) {
+      xv[i] = xr[v];
+      gv[i] = g[v];
+    }
+  }
+  auto sumsq = [](const u32x4 &w) {
+    float t = 0.f;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const float a = bf_lo(w[j]), b = bf_hi(w[j]);
-      ss += a * a + b * b;
+      t += a * a + b * b;
     }
-  }
+    return t;
+  };
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < VPT; ++i)
+    if (threadIdx.x + i * 256 < nvec) ss += sumsq(xv[i]);
+  for (int v = threadIdx.x + VPT * 256; v < nvec; v += 256) ss += sumsq(xr[v]);
   ss = block_sum_256(ss, red);
   const float inv = rsqrtf(ss / (float)H + eps);
   u32x4 *orow = (u32x4 *)(out + row * H);
-  const u32x4 *g = (const u32x4 *)gain;
-  for (int v = threadIdx.x; v < nvec; v += 256) {
-    const u32x4 w = xr[v], gw = g[v];
+  auto scale = [&](const u32x4 &w, const u32x4 &gw) {
     u32x4 o;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       o[j] = pack2(bf_lo(w[j]) * inv * bf_lo(gw[j]), bf_hi(w[j]) * inv * bf_hi(gw[j]));
-    orow[v] = o;
+    return o;
+  };
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int v = threadIdx.x + i * 256;
+    if (v < nvec) orow[v] = scale(xv[i], gv[i]);
   }
+  for (int v = threadIdx.x + VPT * 256; v < nvec; v += 256) orow[v] = scale(xr[v], g[v]);
 }
 
 // One block per (sequence, group of kRopeHeads heads of its qkv row). RoPE

@@ -410,12 +410,8 @@ template <int BM, int BN, int BK, int EPI, bool PARTIAL>
 hipError_t launch_tile(const GemmArgs &a, dim3 grid, hipStream_t s) {
   auto kern = gemm_kernel<BM, BN, BK, 2, 2, EPI, PARTIAL>;
   const size_t lds = lds_bytes(BM, BN, BK, EPI == EPI_SILU);
-  static bool attr_set = false;  // the attribute only raises a per-kernel limit; setting it twice is harmless
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> lds_set{0};  // devices whose limit this kernel already raised
+  if (hipError_t e = ensure_lds_limit((const void *)kern, lds, lds_set); e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, grid, dim3(256), lds, s, a);
   return hipGetLastError();
 }
@@ -424,12 +420,8 @@ template <int BM, int EPI, bool PARTIAL>
 hipError_t launch_big(const GemmArgs &a, dim3 grid, hipStream_t s) {
   auto kern = gemm_big_kernel<BM, EPI, PARTIAL>;
   const size_t lds = (size_t)2 * (BM + 128) * (64 + 8) * 2;
-  static bool attr_set = false;  // the attribute only raises a per-kernel limit; setting it twice is harmless
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> lds_set{0};  // devices whose limit this kernel already raised
+  if (hipError_t e = ensure_lds_limit((const void *)kern, lds, lds_set); e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, grid, dim3(512), lds, s, a);
   return hipGetLastError();
 }

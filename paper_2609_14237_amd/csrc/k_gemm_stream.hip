@@ -304,12 +304,8 @@ hipError_t launch_stream(const GemmArgs &a, hipStream_t s) {
   const dim3 grid = a.group_off ? dim3(n_tiles, a.groups) : dim3(8 * m_tiles * ((n_tiles + g - 1) / g));
   auto kern = gemm_stream_kernel<MG, EPI, PARTIAL>;
   const size_t lds = (size_t)3 * 128 * 64 * 2 + MG * 3 * 64 * 64 * 2;  // 3 B slots + 3 A slots per M group
-  static bool attr_set = false;  // the attribute only raises a per-kernel limit; setting it twice is harmless
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> lds_set{0};  // devices whose limit this kernel already raised
+  if (hipError_t e = ensure_lds_limit((const void *)kern, lds, lds_set); e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, grid, dim3(MG == 4 ? 512 : 256), lds, s, a, n_tiles, m_tiles);
   return hipGetLastError();
 }
