@@ -1,5 +1,6 @@
 """Parity at the full evaluated sizes, in the launch configuration the
-benchmark times (per layer: ops [0,4), [4,5), [5,6), [6,end)). The oracle
+benchmark times (per layer: ops [0,4), [4,5), [5,6), [6,end); tiled weights,
+and row-major weights as well). The oracle
 recomputes a handful of sampled sequences one by one (their pages only).
 
 Two kinds of check:
@@ -67,10 +68,10 @@ def routing_clear(logits, k, gap=3e-2):
 
 
 class FullSize:
-    def __init__(self, w, n_rows):
-        say("full size", w.name, "setup")
+    def __init__(self, w, n_rows, tiled=False):
+        say("full size", w.name, "setup", "tiled" if tiled else "row-major")
         self.w = w
-        self.s = Setup(w, seed=w.seed)
+        self.s = Setup(w, seed=w.seed, tiled=tiled)
         np.testing.assert_array_equal(self.s.page_table,
                                       O.kv_alloc(self.s.ctx, self.s.pool_pages, w.seed, self.s.max_pages))
         self.rows = sample_rows(self.s.ctx, n_rows, 1)
@@ -83,8 +84,8 @@ class FullSize:
         return f64(self.s.buf(name, self.w.batch, width)[self.tr])
 
 
-def _chained(w, n_rows, moe=False):
-    f = FullSize(w, n_rows)
+def _chained(w, n_rows, moe=False, tiled=False):
+    f = FullSize(w, n_rows, tiled)
     s, rows = f.s, f.rows
     inp = f.snapshot()
     say("chained", w.name, "rows", rows)
@@ -168,12 +169,15 @@ def _stages(f, moe=False):
         off += n
 
 
+@pytest.mark.parametrize("tiled", [True, False], ids=["tiled", "rows"])
 @pytest.mark.parametrize("name,n_rows", [("dense8b_b64", 4), ("dense8b_b256_ctx8k", 3), ("hybrid4_b128", 3),
                                          ("moe64x8_b512", 8)])
-def test_fullsize(name, n_rows):
+def test_fullsize(name, n_rows, tiled):
+    """The benchmark runs tiled weights; the row-major layout is the other
+    supported one."""
     w = W.BY_NAME[name]
     moe = w.layers[0].n_experts > 0
-    f = _chained(w, n_rows, moe)
+    f = _chained(w, n_rows, moe, tiled)
     _stages(f, moe)
     del f
     torch.cuda.empty_cache()
