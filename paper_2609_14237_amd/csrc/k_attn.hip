@@ -63,7 +63,7 @@ __device__ __forceinline__ void window_of(int ctx, int window, int &p, int &lo, 
 }
 
 template <int D>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) void attn_flat_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_flat_kernel(
     const uint16_t *__restrict__ qkv, int n_q, int n_kv, int window, const int32_t *__restrict__ ctx_lens,
     const int32_t *__restrict__ page_table, int max_pages, int ring, const uint16_t *__restrict__ pool,
     int64_t pool_pages, int seg_pages, float scale_log2, float *__restrict__ ws_acc, float *__restrict__ ws_ml,
@@ -395,11 +395,12 @@ int num_cus() {
 }
 
 // Grid of the attention kernel: one 4-wave block per compute unit, fewer when
-// the batch cannot fill them with ranges of at least 8 pages. The registers
-// allow three blocks per unit, but fewer waves in flight stream the pool
-// faster: measured on one MI355X, B = 64 x U[512, 4096] 122.7 -> 115.6 us,
-// B = 256 x 8192 1444 -> 1376 us, MoE B = 512 1593 -> 1563 us from three
-// blocks per unit to one (two was in between).
+// the batch cannot fill them with ranges of at least 8 pages. Fewer waves in
+// flight stream the pool faster: measured on one MI355X, B = 64 x U[512, 4096]
+// 122.7 -> 115.6 us, B = 256 x 8192 1444 -> 1376 us, MoE B = 512 1593 ->
+// 1563 us from three blocks per unit to one (two was in between). The kernel
+// is built for at most two waves per SIMD (256 VGPRs), which leaves its 170
+// registers unspilled.
 int attn_grid(int B, int n_kv, int span) {
   const int64_t max_units = (int64_t)B * n_kv * span;
   return (int)std::max<int64_t>(1, std::min<int64_t>(num_cus(), (max_units + 31) / 32));
