@@ -31,6 +31,74 @@ MFMA_BF16_PEAK = 2.5e15    # dense bf16 flop/s, MI355X
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_core_traffic.json")
 
 
+class TimingEvent:
+    """A HIP timing event recorded without the system-scope memory fence
+    (hipEventDisableSystemFence). The default event fences every record with
+    a cache writeback and invalidation, which costs the work that follows it;
+    on one MI355X the decode step measured 0.250 ms with default events at its
+    stage boundaries, 0.243 ms with these, and 0.234 ms with none. Created on
+    the HIP runtime torch has loaded; falls back to torch.cuda.Event elsewhere.
+    Same interface as torch.cuda.Event: record(stream), elapsed_time(other) in ms."""
+    _hip = None
+    _FLAGS = 0x20000000  # hipEventDisableSystemFence (hip_runtime_api.h)
+
+    @classmethod
+    def _runtime(cls):
+        if cls._hip is None:
+            import ctypes as C
+            path = None
+            try:
+                with open("/proc/self/maps") as fh:
+                    for line in fh:
+                        if "libamdhip64" in line:
+                            path = line.split()[-1]
+                            break
+            except OSError:
+                pass
+            if path is None:
+                cls._hip = False
+            else:
+                lib = C.CDLL(path)
+                lib.hipEventCreateWithFlags.argtypes = [C.POINTER(C.c_void_p), C.c_uint]
+                lib.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
+                lib.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+                lib.hipEventDestroy.argtypes = [C.c_void_p]
+                cls._hip = lib
+        return cls._hip
+
+    def __init__(self):
+        import ctypes as C
+        import torch
+        lib = self._runtime()
+        self._torch = None
+        if not lib:
+            self._torch = torch.cuda.Event(enable_timing=True)
+            return
+        self._h = C.c_void_p()
+        if lib.hipEventCreateWithFlags(C.byref(self._h), self._FLAGS) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
+
+    def record(self, stream):
+        import ctypes as C
+        if self._torch is not None:
+            self._torch.record(stream)
+        elif self._runtime().hipEventRecord(self._h, C.c_void_p(stream.cuda_stream)) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_time(self, other) -> float:
+        import ctypes as C
+        if self._torch is not None:
+            return self._torch.elapsed_time(other._torch)
+        ms = C.c_float()
+        if self._runtime().hipEventElapsedTime(C.byref(ms), self._h, other._h) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def __del__(self):
+        if getattr(self, "_torch", 1) is None and self._hip:
+            self._hip.hipEventDestroy(self._h)
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -209,10 +277,10 @@ def ffn_sweep(args):
         times = []
         for i in range(args.steps):
             blk, st = sets[i % copies][:2]
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
+            e0, e1 = TimingEvent(), TimingEvent()
+            e0.record(torch.cuda.current_stream())
             R.run_partition(blk, 6, 10, batch, st, stream)
-            e1.record()
+            e1.record(torch.cuda.current_stream())
             times.append((e0, e1))
         torch.cuda.synchronize()
         t = float(np.median([a.elapsed_time(b) for a, b in times])) * 1e-3
@@ -261,10 +329,10 @@ def latency_table(args):
             fn()
         evs = []
         for _ in range(args.steps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
+            e0, e1 = TimingEvent(), TimingEvent()
+            e0.record(torch.cuda.current_stream())
             fn()
-            e1.record()
+            e1.record(torch.cuda.current_stream())
             evs.append((e0, e1))
         torch.cuda.synchronize()
         return float(np.median([a.elapsed_time(b) for a, b in evs])) * 1e3
@@ -387,7 +455,7 @@ def main():
                 if rc != 0:
                     raise B.OdsError(rc, f"ods_run_partition[{a},{b})")
                 if evs is not None:
-                    evs.append((l, tag, torch.cuda.Event(enable_timing=True)))
+                    evs.append((l, tag, TimingEvent()))
                     evs[-1][2].record(stream)
 
     if args.calib_copy_mib:
@@ -405,13 +473,13 @@ def main():
     torch.cuda.synchronize()
 
     per_step_events = []
-    t_begin = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
+    t_begin = TimingEvent()
+    t_end = TimingEvent()
     torch.cuda.synchronize()
     t_begin.record(stream)
     for i in range(args.steps):
         evs = []
-        start = torch.cuda.Event(enable_timing=True)
+        start = TimingEvent()
         start.record(stream)
         run_step(sets[i % copies], evs)
         per_step_events.append((start, evs))
