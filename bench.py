@@ -472,18 +472,19 @@ def main():
         run_step(sets[i % copies])
     torch.cuda.synchronize()
 
+    # Each step starts at the event that ended the previous one (the timed
+    # region's first event for step 0), so no event sits between two steps.
     per_step_events = []
     t_begin = TimingEvent()
-    t_end = TimingEvent()
     torch.cuda.synchronize()
     t_begin.record(stream)
+    start = t_begin
     for i in range(args.steps):
         evs = []
-        start = TimingEvent()
-        start.record(stream)
         run_step(sets[i % copies], evs)
         per_step_events.append((start, evs))
-    t_end.record(stream)
+        start = evs[-1][2]
+    t_end = start
     torch.cuda.synchronize()
     total_ms = t_begin.elapsed_time(t_end)
     ms_per_step = total_ms / args.steps
