@@ -379,7 +379,7 @@ def latency_table(args):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(collectives and sharding are out of scope); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
     if args.ffn_sweep:

@@ -5,7 +5,7 @@
 // as the LDS image of each K step's tile, read as one contiguous run per
 // block): C[m, n] = sum_k A[m, k] * B[n, k] with the same epilogues as the
 // other GEMM kernels. Built on its own with MFMA results in
-// VGPRs (the build passes -amdgpu-mfma-vgpr-form for this file only), which
+// VGPRs (build.py passes -amdgpu-mfma-vgpr-form for this file only), which
 // keeps the accumulators in place across the K loop.
 #include <algorithm>
 #include <type_traits>
