@@ -129,7 +129,8 @@ typedef struct {
 /* Per-step metadata (device pointers). ctx_lens[b] counts the keys sequence b
  * attends to, the token being decoded included, so that token's position is
  * ctx_lens[b] - 1; valid values are 1 .. max_pages * 16 (larger values are
- * clamped, values < 1 make the row a no-op for attention and KV append).
+ * clamped; a row with a value < 1 is left alone by RoPE and KV append, and
+ * its attention output is a row of zeros).
  * page_table [batch][max_pages] int32, -1 for unused entries; page ids outside
  * [0, pool_pages) are skipped by the kernels. attn_core numbers the (sequence,
  * KV head, window page) units of the batch and gives every wave of its grid an
@@ -241,7 +242,9 @@ const char *ods_op_name(const ods_block *blk, int32_t op);
  * submission for one stage; Section 6). Adjacent operators inside the range
  * may be fused; every buffer of the live set at op_end is materialised, so a
  * block run as any sequence of contiguous ranges computes the same step.
- * ODS_ERANGE unless 0 <= op_begin < op_end <= ods_block_num_ops(). */
+ * ODS_ERANGE unless 0 <= op_begin < op_end <= ods_block_num_ops(). An empty
+ * batch (batch->batch == 0) returns ODS_OK once the block and the range are
+ * valid, enqueueing nothing and reading no pointer of batch or state. */
 ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_end,
                              const ods_batch *batch, ods_state *state, hipStream_t stream);
 

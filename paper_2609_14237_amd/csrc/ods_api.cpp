@@ -270,6 +270,10 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
   if (B < 0) return fail(ODS_EINVAL, "negative batch");
   if (batch->split_pages < 0) return fail(ODS_EINVAL, "negative split_pages");
   if (batch->ring_pages < 0) return fail(ODS_EINVAL, "negative ring_pages");
+  if (B == 0) {  // nothing to read or write: the batch-sized pointers may be null
+    g_err[0] = 0;
+    return ODS_OK;
+  }
 
   // ---- validation pass: every pointer an operator in the range touches ----
   std::vector<OpRef> ops;
@@ -357,16 +361,11 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
     if (o.kind == K_ATTN_CORE || o.kind == K_QKV || o.kind == K_O_PROJ || o.kind == K_GATE_UP ||
         o.kind == K_DOWN || o.kind == K_ROUTER)
       uses_ws = true;
-  if (uses_ws && B > 0) {
+  if (uses_ws) {
     if (!st->ws) return fail(ODS_EINVAL, "ws is null");
     if (st->ws_bytes < ws_need)
       return fail(ODS_ENOMEM, "workspace %zu bytes < required %zu", st->ws_bytes, ws_need);
   }
-  if (B == 0) {
-    g_err[0] = 0;
-    return ODS_OK;
-  }
-
   // ---- dispatch ----
   const bool trace = trace_on();
   auto U = [](const void *p) { return (uint16_t *)p; };
