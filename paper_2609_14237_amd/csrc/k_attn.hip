@@ -383,15 +383,15 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float *__restrict
 
 // Compute units of the current device (queried once per process and device).
 int num_cus() {
-  static int cached[64] = {0};
+  static std::atomic<int> cached[64] = {};  // 0: not queried yet (threads may race to fill a slot, same value)
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (!cached[dev]) {
-    int n = 0;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cached[dev] = n;
+    cached[dev].store(n, std::memory_order_relaxed);
   }
-  return cached[dev];
+  return n;
 }
 
 // Grid of the attention kernel: one 4-wave block per compute unit, fewer when
