@@ -339,6 +339,9 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float *__restrict
   // empty sequence is never used).
   const int ctx = ctx_lens[b];
   const int2 meta = ws_meta[(int64_t)b * n_kv + h / group];
+  // Keeps the metadata load ahead of the context test (the compiler would
+  // otherwise sink it past the branch and wait for the context first).
+  asm volatile("" ::"v"(meta.x), "v"(meta.y));
   if (ctx < 1) {
 #pragma unroll
     for (int i = 0; i < DPL; ++i) dst[i] = 0;
@@ -347,6 +350,19 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float *__restrict
   const int n_seg = meta.y;
   if (n_seg <= 1) return;  // written by the attention kernel
   const int64_t rec0 = (int64_t)meta.x * group + h % group;  // records rec0 + c * group
+  // The accumulators of the first kPre records load together with the (m, l)
+  // pairs (neither depends on the other), so a sequence split a few ways costs
+  // one round trip after the metadata instead of two.
+  constexpr int kPre = 4;
+  float pre[kPre][DPL];
+#pragma unroll
+  for (int c = 0; c < kPre; ++c) {
+    if (c < n_seg) {
+      const float *src = ws_acc + (rec0 + (int64_t)c * group) * D + lane * DPL;
+#pragma unroll
+      for (int i = 0; i < DPL; ++i) pre[c][i] = src[i];
+    }
+  }
   // (m, l) of record c as one 8-byte load; lane c keeps record c (< 64).
   auto ml_of = [&](int c) { return *(const float2 *)(ws_ml + (rec0 + (int64_t)c * group) * 2); };
   const float2 own = lane < n_seg ? ml_of(lane) : make_float2(-INFINITY, 0.f);
@@ -363,7 +379,18 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float *__restrict
   float acc[DPL];
 #pragma unroll
   for (int i = 0; i < DPL; ++i) acc[i] = 0.f;
-  for (int c0 = 0; c0 < n_seg; c0 += 64) {
+  if (n_seg <= kPre) {
+    const float wl = lane < n_seg ? weight_of(own.x) : 0.f;
+#pragma unroll
+    for (int c = 0; c < kPre; ++c) {
+      if (c < n_seg) {
+        const float w = __shfl(wl, c, kWave);
+#pragma unroll
+        for (int i = 0; i < DPL; ++i) acc[i] += w * pre[c][i];
+      }
+    }
+  }
+  for (int c0 = 0; n_seg > kPre && c0 < n_seg; c0 += 64) {
     const float wl = (c0 + lane < n_seg) ? (c0 == 0 ? weight_of(own.x) : weight_of(ml_of(c0 + lane).x)) : 0.f;
     const int n = min(64, n_seg - c0);
 #pragma unroll 4
