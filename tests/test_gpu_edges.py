@@ -1,8 +1,8 @@
 """Degenerate inputs of the decode path on the GPU, through the C ABI.
 
 - An empty batch (batch = 0) enqueues nothing: every live buffer, the
-  workspace-fed outputs and the KV pool keep their bytes, for whole layers and
-  for the stage entry points.
+  workspace-fed outputs and the KV pool keep their bytes, for whole layers,
+  the stage entry points and a graph captured at batch 0.
 - Rows with no context (ctx_lens < 1) are no-ops for KV append and attention:
   their attention output is exactly zero, so the attention stage leaves their
   residual rows unchanged; the pool keeps every byte outside the slots the
@@ -63,6 +63,13 @@ def test_empty_batch_enqueues_nothing(wl):
     s.R.attn_stage(s.block, 0, empty, s.state)
     s.R.ffn_stage(s.block, 0, empty, s.state)
     torch.cuda.synchronize()
+    assert_unchanged(s, snap)
+    # a graph captured at batch 0 holds no work: replays leave every byte alone
+    g = s.R.PartitionGraph(s.block, 0, n, empty, s.state)
+    for _ in range(2):
+        g.launch()
+        torch.cuda.synchronize()
+    g.close()
     assert_unchanged(s, snap)
 
 
