@@ -79,54 +79,29 @@ __global__ __launch_bounds__(256) void rope_append_kernel(uint16_t *qkv, int n_q
   const int nh = n_q + 2 * n_kv, W = nh * D;
   const int h0 = blockIdx.y * kRopeHeads, h1 = min(nh, h0 + kRopeHeads);
   uint16_t *row = qkv + (int64_t)b * W;
-  // With splits > 1, the columns of heads [h0, h1) = bf16(sum over s of
-  // partial[s][b]), splits in order from zero: what the split-K reduce would
-  // have written. kRopeHeads * D <= 1024 columns, so each thread owns at most
-  // one 4-column group. Its first eight splits' loads go out together, then
-  // the (scalar) loads of the context and its page id, so the three overlap.
-  int ctx, p, page = -1;
-  auto load_slot = [&]() {
-    ctx = ctx_lens[b];
-    p = (ring > 0 ? ctx : min(ctx, max_pages * kPage)) - 1;
-    if (do_append && ctx >= 1) page = page_table[(int64_t)b * max_pages + (ring > 0 ? (p / kPage) % ring : p / kPage)];
-  };
   if (splits > 1) {
-    // Threads past the group's columns load column group h0 D again and store
-    // nothing; splits past the last re-read it (an L1 hit). Unconditional
-    // loads keep the compiler from waiting on each one.
-    const int c0 = h0 * D + threadIdx.x * 4;
-    const bool own_c = c0 < h1 * D;
-    const int c = own_c ? c0 : h0 * D;
-    f32x4 pv[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) pv[j] = *(const f32x4 *)(partial + ((int64_t)min(j, splits - 1) * B + b) * W + c);
-    load_slot();
-    f32x4 v = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int j = 0; j < 8; ++j) v = j < splits ? v + pv[j] : v;
-    for (int s0 = 8; s0 < splits; s0 += 8) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) pv[j] = *(const f32x4 *)(partial + ((int64_t)min(s0 + j, splits - 1) * B + b) * W + c);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) v = s0 + j < splits ? v + pv[j] : v;
-    }
-    if (own_c) {
+    // columns of heads [h0, h1) = bf16(sum over s of partial[s][b]), 4 per
+    // thread, splits in order: what the split-K reduce would have written.
+    for (int c = h0 * D + threadIdx.x * 4; c < h1 * D; c += 256 * 4) {
+      f32x4 v = {0.f, 0.f, 0.f, 0.f};
+      for (int sp = 0; sp < splits; ++sp) v += *(const f32x4 *)(partial + ((int64_t)sp * B + b) * W + c);
       u32x2 o;
       o[0] = pack2(v[0], v[1]);
       o[1] = pack2(v[2], v[3]);
       *(u32x2 *)(row + c) = o;
     }
     __syncthreads();  // the columns are read back below by other threads of this block
-  } else {
-    load_slot();
   }
+  const int ctx = ctx_lens[b];
   if (ctx < 1) return;
+  const int p = (ring > 0 ? ctx : min(ctx, max_pages * kPage)) - 1;
   const int half = D / 2, nvh = half / 8;
 
   uint16_t *kbase = nullptr, *vbase = nullptr;
   const int64_t blk = (int64_t)kPage * D;
   const int slot = p % kPage;
   if (do_append) {
+    const int page = page_table[(int64_t)b * max_pages + (ring > 0 ? (p / kPage) % ring : p / kPage)];
     if (page >= 0 && page < pool_pages) {
       kbase = pool + (int64_t)page * 2 * n_kv * blk;
       vbase = kbase + n_kv * blk;

@@ -375,35 +375,19 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs p) {
   if (q * 4 >= total) return;
   const int m = (int)(q * 4 / p.N), n = (int)(q * 4 % p.N);
   const int64_t ncols = EPI == EPI_SILU ? 2 * (int64_t)p.N : p.N;
-  uint16_t *c = (uint16_t *)p.C + (int64_t)m * p.ldc + n;
-  u32x2 old = {0u, 0u};
-  if (EPI == EPI_RESID) old = *(const u32x2 *)c;
-  // Splits are summed in order from zero; their loads go out eight at a time
-  // (a loop of dependent load-add pairs would wait one round trip per split).
   f32x4 v = {0.f, 0.f, 0.f, 0.f}, up = {0.f, 0.f, 0.f, 0.f};
-  for (int s0 = 0; s0 < p.splits; s0 += 8) {
-    f32x4 pv[8], pu[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      if (s0 + j < p.splits) {
-        const float *row = p.partial + ((int64_t)(s0 + j) * p.M + m) * ncols;
-        pv[j] = *(const f32x4 *)(row + n);
-        if (EPI == EPI_SILU) pu[j] = *(const f32x4 *)(row + p.N + n);
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      if (s0 + j < p.splits) {
-        v += pv[j];
-        if (EPI == EPI_SILU) up += pu[j];
-      }
-    }
+  for (int s = 0; s < p.splits; ++s) {
+    const float *row = p.partial + ((int64_t)s * p.M + m) * ncols;
+    v += *(const f32x4 *)(row + n);
+    if (EPI == EPI_SILU) up += *(const f32x4 *)(row + p.N + n);
   }
   if (EPI == EPI_F32) {
     *(f32x4 *)((float *)p.C + (int64_t)m * p.ldc + n) = v;
     return;
   }
+  uint16_t *c = (uint16_t *)p.C + (int64_t)m * p.ldc + n;
   if (EPI == EPI_RESID) {
+    const u32x2 old = *(const u32x2 *)c;
     v[0] += bf_lo(old[0]);
     v[1] += bf_hi(old[0]);
     v[2] += bf_lo(old[1]);
