@@ -258,3 +258,14 @@ def test_tiled_layout_validation():
     ok = fake_block(W.DENSE_8B_B64.layers)
     ok._layers[0].weight_layout = B.ODS_WEIGHTS_TILED
     assert B.ods_workspace_bytes(ok.c, fake_batch(64, 256)) > 0
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """The benchmark measures one GPU; --gpus N > 1 exits with a message before
+    touching a device."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120, cwd=ROOT)
+    assert r.returncode != 0
+    assert "one GPU" in (r.stdout + r.stderr)
