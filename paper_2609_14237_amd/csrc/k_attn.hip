@@ -182,10 +182,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       R.p = ip;
       R.ok = live && (unsigned)page < (unsigned long long)pool_pages;
       const uint16_t *kb = pool + (int64_t)ig * BLK + (int64_t)(R.ok ? page : 0) * page_stride;
+      // K/V bytes are read once per launch: non-temporal loads (the nt cache
+      // policy) stream them past the caches instead of evicting the q rows,
+      // page ids and records the kernel does reuse (B = 64: 115 -> 103 us).
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) R.k[kk] = *(const u32x4 *)(kb + hl * D + kk * 32 + rq * 8);
+      for (int kk = 0; kk < KK; ++kk)
+        R.k[kk] = __builtin_nontemporal_load((const u32x4 *)(kb + hl * D + kk * 32 + rq * 8));
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) R.v[nb] = *(const u32x2 *)(kb + v_off + (nb * 16 + hl) * kPage + rq * 4);
+      for (int nb = 0; nb < NB; ++nb)
+        R.v[nb] = __builtin_nontemporal_load((const u32x2 *)(kb + v_off + (nb * 16 + hl) * kPage + rq * 4));
       const uint16_t *qp = qkv + (int64_t)ib * row_elems + (int64_t)(ig * group + (head_ok ? hl : 0)) * D;
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) R.q[kk] = *(const u32x4 *)(qp + kk * 32 + rq * 8);
