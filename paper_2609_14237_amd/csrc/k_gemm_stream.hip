@@ -98,10 +98,12 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
   // When a weight tile is read by exactly one block, once (a dense GEMM with
   // one M tile, an expert whose rows fit one tile), its loads carry the
   // non-temporal policy, so the weight stream does not evict the activation
-  // rows every block re-reads (B = 64: gate_up + down 85 -> 73 us). Weight
-  // tiles shared by the M tiles of one XCD keep the default policy: the L2
-  // serves their re-reads.
-  const bool b_once = p.group_off ? m_last - m_first <= BM : m_tiles == 1;
+  // rows every block re-reads (B = 64: gate_up 43 -> 40 us, down 27.5 -> 26
+  // us). Weight tiles shared by the M tiles of one XCD keep the default
+  // policy (the L2 serves their re-reads), and so do the split-K blocks of
+  // the 256-row tile, which measured slower with it (down at B = 256: 34 ->
+  // 46 us).
+  const bool b_once = (MG == 1 || p.splits == 1) && (p.group_off ? m_last - m_first <= BM : m_tiles == 1);
 
   const int steps = p.K / BK;
   const int per = (steps + p.splits - 1) / p.splits;
