@@ -248,6 +248,29 @@ const char *ods_op_name(const ods_block *blk, int32_t op);
 ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_end,
                              const ods_batch *batch, ods_state *state, hipStream_t stream);
 
+/* Size of the workspace the library itself holds on each device for
+ * ods_run_partition_scratch (64 MiB; every evaluated block needs at most
+ * 40 MiB, as ods_workspace_bytes reports). */
+#define ODS_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops and harnesses that forbid hipMalloc): the same as
+ * ods_run_partition, except that the workspace is a static device array of
+ * ODS_SCRATCH_BYTES bytes inside the library instead of state->ws (state->ws
+ * and state->ws_bytes are ignored and may be NULL / 0). The caller still
+ * passes every input and output buffer. Nothing is allocated or freed: each
+ * device the library runs on holds its own copy of the array from module load
+ * until the process ends; its address is resolved on the first call on a
+ * device (with that device current). Nothing in the array needs to start at
+ * zero; it keeps the contents the last call left. Calls that overlap on one
+ * GPU (several streams or threads at once) share the array and race: the
+ * caller must order them, e.g. on one stream per device.
+ * Errors: those of ods_run_partition, plus ODS_ENOMEM when the range needs
+ * more than ODS_SCRATCH_BYTES of workspace (nothing is enqueued) and ODS_EHIP
+ * when the array's device address cannot be resolved. */
+ods_status ods_run_partition_scratch(const ods_block *blk, int32_t op_begin, int32_t op_end,
+                                     const ods_batch *batch, ods_state *state, hipStream_t stream);
+
 /* The attention stage of layer `layer`: its operators 0..5 (attention-FFN
  * disaggregation's attention side; Section 2, "Attention-FFN Disaggregation"). */
 ods_status ods_attn_stage(const ods_block *blk, int32_t layer, const ods_batch *batch,

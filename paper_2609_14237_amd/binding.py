@@ -16,6 +16,7 @@ ODS_OK, ODS_EINVAL, ODS_ERANGE, ODS_ENOMEM, ODS_EUNSUPPORTED, ODS_EHIP = 0, -1, 
 STATUS_NAMES = {0: "ODS_OK", -1: "ODS_EINVAL", -2: "ODS_ERANGE", -3: "ODS_ENOMEM",
                 -4: "ODS_EUNSUPPORTED", -5: "ODS_EHIP"}
 PAGE_TOKENS = 16
+SCRATCH_BYTES = 64 << 20  # ODS_SCRATCH_BYTES
 ODS_WEIGHTS_ROWS, ODS_WEIGHTS_TILED = 0, 1
 
 BUFFERS = ("resid", "xn", "qkv", "o", "hn", "gu", "act", "logits", "topk_w", "topk_ids", "perm",
@@ -66,6 +67,8 @@ SIGNATURES = {
     "ods_op_name": (C.c_char_p, [C.POINTER(ods_block), C.c_int32]),
     "ods_run_partition": (C.c_int, [C.POINTER(ods_block), C.c_int32, C.c_int32, C.POINTER(ods_batch),
                                     C.POINTER(ods_state), C.c_void_p]),
+    "ods_run_partition_scratch": (C.c_int, [C.POINTER(ods_block), C.c_int32, C.c_int32, C.POINTER(ods_batch),
+                                            C.POINTER(ods_state), C.c_void_p]),
     "ods_attn_stage": (C.c_int, [C.POINTER(ods_block), C.c_int32, C.POINTER(ods_batch),
                                  C.POINTER(ods_state), C.c_void_p]),
     "ods_ffn_stage": (C.c_int, [C.POINTER(ods_block), C.c_int32, C.POINTER(ods_batch),
@@ -141,6 +144,11 @@ def ods_op_name(blk: ods_block, op: int):
 def ods_run_partition(blk: ods_block, op_begin: int, op_end: int, batch: ods_batch, state: ods_state,
                       stream: int) -> int:
     return lib.ods_run_partition(C.byref(blk), op_begin, op_end, C.byref(batch), C.byref(state), stream)
+
+
+def ods_run_partition_scratch(blk: ods_block, op_begin: int, op_end: int, batch: ods_batch, state: ods_state,
+                              stream: int) -> int:
+    return lib.ods_run_partition_scratch(C.byref(blk), op_begin, op_end, C.byref(batch), C.byref(state), stream)
 
 
 def ods_attn_stage(blk: ods_block, layer: int, batch: ods_batch, state: ods_state, stream: int) -> int:

@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -159,6 +160,49 @@ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 bool trace_on() {
   const char *e = getenv("ODS_TRACE");
   return e && e[0] && e[0] != '0';
+}
+
+size_t range_ws_bytes(const ods_block *blk, int op_begin, int op_end, const ods_batch *batch) {
+  size_t w = 0;
+  for (int g = op_begin; g < op_end; ++g) w = std::max(w, layer_ws_bytes(blk->layers[op_at(blk, g).layer], batch));
+  return w;
+}
+
+}  // namespace
+
+// Workspace held by the library for callers that cannot allocate device
+// memory (ods_run_partition_scratch). Each device the library runs on holds
+// its own copy, zero-filled at load, until the process ends. In host code
+// this name is a host-side stand-in, never a device address: the address is
+// resolved per device with hipGetSymbolAddress and only that pointer is
+// passed to kernels.
+static __device__ __align__(256) uint8_t scratch[ODS_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxScratchDevices] = {};
+
+// Device address of `scratch` on the current device, resolved on the first
+// call per device (with that device current) and cached.
+ods_status scratch_ptr(void **out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(ODS_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(ODS_EUNSUPPORTED, "device %d: the library scratch supports device ids below %d", dev,
+                kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(ODS_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return ODS_OK;
 }
 
 }  // namespace
@@ -354,8 +398,7 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
     }
     if (is_moe(c) && (int64_t)B * c.top_k > INT32_MAX / 2) return fail(ODS_ERANGE, "batch * top_k too large");
   }
-  size_t ws_need = 0;
-  for (auto &o : ops) ws_need = std::max(ws_need, layer_ws_bytes(blk->layers[o.layer], batch));
+  const size_t ws_need = range_ws_bytes(blk, op_begin, op_end, batch);
   bool uses_ws = false;
   for (auto &o : ops)
     if (o.kind == K_ATTN_CORE || o.kind == K_QKV || o.kind == K_O_PROJ || o.kind == K_GATE_UP ||
@@ -494,6 +537,30 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
   }
   g_err[0] = 0;
   return ODS_OK;
+}
+
+ods_status ods_run_partition_scratch(const ods_block *blk, int32_t op_begin, int32_t op_end,
+                                     const ods_batch *batch, ods_state *state, hipStream_t stream) {
+  ods_status rc = check_block(blk);
+  if (rc != ODS_OK) return rc;
+  if (!batch || !state) return fail(ODS_EINVAL, "null batch or state");
+  const int n_ops = num_ops(blk);
+  if (op_begin < 0 || op_end > n_ops || op_begin >= op_end)
+    return fail(ODS_ERANGE, "operator range [%d, %d) outside [0, %d) or empty", op_begin, op_end, n_ops);
+  if (batch->batch < 0 || batch->split_pages < 0 || batch->ring_pages < 0)
+    return fail(ODS_EINVAL, "negative batch, split_pages or ring_pages");
+  ods_state st = *state;
+  st.ws = nullptr;
+  st.ws_bytes = 0;
+  if (batch->batch == 0) return ods_run_partition(blk, op_begin, op_end, batch, &st, stream);
+  const size_t need = range_ws_bytes(blk, op_begin, op_end, batch);
+  if (need > ODS_SCRATCH_BYTES)
+    return fail(ODS_ENOMEM, "operators [%d, %d) need %zu bytes of workspace; the library scratch holds %zu",
+                op_begin, op_end, need, (size_t)ODS_SCRATCH_BYTES);
+  rc = scratch_ptr(&st.ws);
+  if (rc != ODS_OK) return rc;
+  st.ws_bytes = ODS_SCRATCH_BYTES;
+  return ods_run_partition(blk, op_begin, op_end, batch, &st, stream);
 }
 
 size_t ods_tiled_weight_bytes(int32_t out, int32_t in, int32_t gated, int32_t groups) {

@@ -157,6 +157,14 @@ def run_partition(block: DeviceBlock, op_begin: int, op_end: int, batch: DeviceB
     _b._check(st, f"ods_run_partition[{op_begin},{op_end})")
 
 
+def run_partition_scratch(block: DeviceBlock, op_begin: int, op_end: int, batch: DeviceBatch, state: DeviceState,
+                          stream: int | None = None) -> None:
+    """ods_run_partition_scratch: the same range on the library's own workspace (state.ws is not used)."""
+    st = _b.ods_run_partition_scratch(block.c, op_begin, op_end, batch.c, state.c,
+                                      current_stream() if stream is None else stream)
+    _b._check(st, f"ods_run_partition_scratch[{op_begin},{op_end})")
+
+
 def attn_stage(block, layer, batch, state, stream=None) -> None:
     st = _b.ods_attn_stage(block.c, layer, batch.c, state.c, current_stream() if stream is None else stream)
     _b._check(st, f"ods_attn_stage({layer})")

@@ -269,3 +269,21 @@ def test_bench_refuses_more_than_one_gpu():
                        text=True, timeout=120, cwd=ROOT)
     assert r.returncode != 0
     assert "one GPU" in (r.stdout + r.stderr)
+
+
+def test_scratch_entry_point_validates_before_touching_the_device():
+    """ods_run_partition_scratch rejects what ods_run_partition rejects, and a
+    range whose workspace exceeds the library's scratch, before any device call."""
+    blk = fake_block(W.TINY.layers)
+    assert B.ods_run_partition_scratch(blk.c, 0, 0, fake_batch(), fake_state(), 0) == B.ODS_ERANGE
+    assert B.lib.ods_run_partition_scratch(C.byref(blk.c), 0, 4, None, C.byref(fake_state()), 0) == B.ODS_EINVAL
+    # the 8B-shaped layer at batch 4096 needs more than the 64 MiB the library holds
+    big = fake_block(W.DENSE_8B_B256.layers)
+    batch = fake_batch(4096, 512)
+    assert B.ods_workspace_bytes(big.c, batch) > B.SCRATCH_BYTES
+    assert B.ods_run_partition_scratch(big.c, 0, 10, batch, fake_state(ws=None, ws_bytes=0), 0) == B.ODS_ENOMEM
+    assert "scratch" in B.ods_last_error()
+    # every evaluated block fits
+    for w in W.ALL:
+        blk = fake_block(w.layers)
+        assert 0 < B.ods_workspace_bytes(blk.c, fake_batch(w.batch, w.max_pages)) <= B.SCRATCH_BYTES, w.name
