@@ -97,16 +97,19 @@ def kv_alloc(ctx_lens, pool_pages: int, seed: int, max_pages: int) -> np.ndarray
 # (page, 1, g) holds the values dim-major (dim i, slot t at i * 16 + t).
 # ----------------------------------------------------------------------------
 
-def page_kv(pool: np.ndarray, page_row, n_tokens: int, n_kv: int, d: int):
-    """Keys and values of token positions [0, n_tokens) of one sequence:
-    K, V each [n_kv, n_tokens, d] float64."""
-    n_pages = -(-n_tokens // PAGE)
-    pages = np.asarray(page_row[:n_pages], dtype=np.int64)
+def page_kv(pool: np.ndarray, page_row, n_tokens: int, n_kv: int, d: int, first: int = 0):
+    """Keys and values of token positions [first, n_tokens) of one sequence:
+    K, V each [n_kv, n_tokens - first, d] float64. Only the pages holding
+    those positions are read."""
+    p0 = first // PAGE
+    n_pages = -(-n_tokens // PAGE) - p0
+    pages = np.asarray(page_row[p0:p0 + n_pages], dtype=np.int64)
     blk = np.asarray(pool[pages], dtype=np.float64)            # [np, 2, n_kv, 16 d]
     K = blk[:, 0].reshape(n_pages, n_kv, PAGE, d).transpose(1, 0, 2, 3)
     V = blk[:, 1].reshape(n_pages, n_kv, d, PAGE).transpose(1, 0, 3, 2)
-    K = K.reshape(n_kv, n_pages * PAGE, d)[:, :n_tokens]
-    V = V.reshape(n_kv, n_pages * PAGE, d)[:, :n_tokens]
+    t0 = first - p0 * PAGE
+    K = K.reshape(n_kv, n_pages * PAGE, d)[:, t0:t0 + n_tokens - first]
+    V = V.reshape(n_kv, n_pages * PAGE, d)[:, t0:t0 + n_tokens - first]
     return K, V
 
 
@@ -170,6 +173,20 @@ def silu(z: np.ndarray) -> np.ndarray:
     return z / (1.0 + np.exp(-z))
 
 
+def route_weights(logits: np.ndarray, ids: np.ndarray) -> np.ndarray:
+    """Routing weights of a given expert choice: the softmax probabilities of
+    the chosen experts renormalised over them ([B, k] float64). topk_route
+    applies the same formula to its own choice."""
+    out = np.empty(np.shape(ids))
+    for b in range(out.shape[0]):
+        z = np.asarray(logits[b], dtype=np.float64)
+        p = np.exp(z - z.max())
+        p = p / p.sum()
+        chosen = p[np.asarray(ids[b], dtype=np.int64)]
+        out[b] = chosen / chosen.sum()
+    return out
+
+
 def topk_route(logits: np.ndarray, k: int):
     """Softmax over all experts, top-k by probability with ties to the lower
     index, weights renormalised over the chosen k. Returns (ids int32 [B,k],
@@ -219,8 +236,10 @@ def run_ops(cfgs, weights, pools, page_table, ctx_lens, live: dict, op_begin: in
     cfgs: per-layer configs; weights: per-layer dicts of float64 arrays (same
     names and layouts as the library's weights); pools: per-layer float64 KV
     pools [P, 2, n_kv, 16 d] (updated in place by kv_append); page_table
-    [B, max_pages] int; ctx_lens [B]; live: dict of float64/int arrays keyed by
-    live-buffer name (updated and returned).
+    [B, max_pages] int, or a list with one such table per layer (each indexing
+    that layer's pool); ctx_lens [B]; live: dict of float64/int arrays keyed by
+    live-buffer name (updated and returned). A sliding-window layer reads only
+    the pages of its window, so its table may leave the others at -1.
     """
     ops = block_op_list(cfgs)
     if not (0 <= op_begin < op_end <= len(ops)):
@@ -230,6 +249,7 @@ def run_ops(cfgs, weights, pools, page_table, ctx_lens, live: dict, op_begin: in
     B = ctx.shape[0]
     for (l, _, name) in ops[op_begin:op_end]:
         cfg, w, pool = cfgs[l], weights[l], pools[l]
+        table = page_table[l] if isinstance(page_table, (list, tuple)) else page_table
         H, nq, nkv, d = cfg.hidden, cfg.n_q, cfg.n_kv, cfg.head_dim
         if name == "attn_norm":
             live["xn"] = rmsnorm(live["resid"], w["g_attn"], cfg.rms_eps)
@@ -248,14 +268,15 @@ def run_ops(cfgs, weights, pools, page_table, ctx_lens, live: dict, op_begin: in
                 p = int(pos[b])
                 k = qkv[b, nq * d:(nq + nkv) * d].reshape(nkv, d)
                 v = qkv[b, (nq + nkv) * d:].reshape(nkv, d)
-                write_kv_slot(pool, int(page_table[b, p // PAGE]), p % PAGE, k, v, d)
+                write_kv_slot(pool, int(table[b, p // PAGE]), p % PAGE, k, v, d)
         elif name == "attn_core":
             o = np.empty((B, nq * d))
             for b in range(B):
                 p = int(pos[b])
-                K, V = page_kv(pool, page_table[b], p + 1, nkv, d)
+                lo = window_start(p, cfg.window)
+                K, V = page_kv(pool, table[b], p + 1, nkv, d, first=lo)   # keys lo .. p
                 q = live["qkv"][b, :nq * d].reshape(nq, d)
-                o[b] = attention_row(q, K, V, window_start(p, cfg.window), p).reshape(-1)
+                o[b] = attention_row(q, K, V, 0, p - lo).reshape(-1)
             live["o"] = o
         elif name == "o_proj_residual":
             live["resid"] = live["resid"] + linear(live["o"], w["w_o"])

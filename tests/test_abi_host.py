@@ -287,3 +287,23 @@ def test_scratch_entry_point_validates_before_touching_the_device():
     for w in W.ALL:
         blk = fake_block(w.layers)
         assert 0 < B.ods_workspace_bytes(blk.c, fake_batch(w.batch, w.max_pages)) <= B.SCRATCH_BYTES, w.name
+
+
+def test_kv_alloc_worked_example_in_the_library():
+    """The library's allocator reproduces the specification's worked example
+    (tests/golden/kv_alloc_worked_example.txt), independently of the oracle."""
+    rows = [l.split() for l in open(os.path.join(ROOT, "tests", "golden", "kv_alloc_worked_example.txt"))
+            if l.strip() and not l.startswith("#")]
+    ex = {}
+    pages = []
+    for key, *vals in rows:
+        if key == "pages":
+            pages.append([int(v) for v in vals])
+        else:
+            ex[key] = [int(v, 0) for v in vals]
+    ctx = np.array(ex["contexts"], dtype=np.int32)
+    table = np.zeros((len(ctx), 3), dtype=np.int32)
+    assert B.ods_kv_alloc(ex["pool_pages"][0], ctx, len(ctx), ex["seed"][0], 3, table) == B.ODS_OK
+    for b, want in enumerate(pages):
+        assert table[b, :len(want)].tolist() == want
+        assert (table[b, len(want):] == -1).all()

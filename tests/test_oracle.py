@@ -52,6 +52,34 @@ def test_fisher_yates_small_case_by_hand():
     assert O.page_permutation(3, 7) == perm
 
 
+def load_kv_alloc_example():
+    ex = {"pages": []}
+    for line in open(os.path.join(GOLDEN, "kv_alloc_worked_example.txt")):
+        if not line.strip() or line.startswith("#"):
+            continue
+        key, *vals = line.split()
+        vals = [int(v, 0) for v in vals]
+        if key == "pages":
+            ex["pages"].append(vals)
+        else:
+            ex[key] = vals
+    return ex
+
+
+def test_kv_alloc_worked_example():
+    ex = load_kv_alloc_example()
+    state = 0
+    for want in ex["splitmix64_seed0"]:
+        state, out = O.splitmix64(state)
+        assert out == want
+    P, seed = ex["pool_pages"][0], ex["seed"][0]
+    assert O.page_permutation(P, seed) == ex["permutation"]
+    table = O.kv_alloc(ex["contexts"], P, seed, 3)
+    for b, pages in enumerate(ex["pages"]):
+        np.testing.assert_array_equal(table[b, :len(pages)], pages)
+        assert (table[b, len(pages):] == -1).all()
+
+
 @pytest.mark.parametrize("seed", [0, 1, 12345])
 def test_kv_alloc_invariants(seed):
     rng = np.random.default_rng(seed)
@@ -156,6 +184,13 @@ def test_page_gather_matches_logical_layout():
         K, V = O.page_kv(pool, table[b], c, n_kv, d)
         np.testing.assert_array_equal(K, Ks[b])
         np.testing.assert_array_equal(V, Vs[b])
+        # a window [first, c) reads only its own pages and returns those positions
+        for first in sorted({0, 1, 15, 16, 17, c - 1} & set(range(c))):
+            sub = table[b].copy()
+            sub[:first // 16] = -1          # pages before the window are never read
+            K, V = O.page_kv(pool, sub, c, n_kv, d, first=first)
+            np.testing.assert_array_equal(K, Ks[b][:, first:])
+            np.testing.assert_array_equal(V, Vs[b][:, first:])
 
 
 def test_attention_invariants():
@@ -217,6 +252,20 @@ def test_topk_matches_stable_argsort_and_ties():
     for b in range(50):
         z = logits[b][ids[b]]
         np.testing.assert_allclose(w[b], np.exp(z - z.max()) / np.exp(z - z.max()).sum(), rtol=1e-13)
+
+
+def test_route_weights_of_a_given_choice():
+    rng = np.random.default_rng(14)
+    logits = rng.normal(size=(30, 12))
+    ids, w = O.topk_route(logits, 3)
+    np.testing.assert_allclose(O.route_weights(logits, ids), w, rtol=1e-14)
+    # any choice: exp(z_i) / sum over the chosen exp(z_j), summing to one
+    other = np.stack([rng.permutation(12)[:3] for _ in range(30)])
+    got = O.route_weights(logits, other)
+    for b in range(30):
+        e = np.array([math.exp(logits[b, i]) for i in other[b]])
+        np.testing.assert_allclose(got[b], e / e.sum(), rtol=1e-13)
+    np.testing.assert_allclose(got.sum(axis=1), 1.0, rtol=1e-14)
 
 
 def test_permute_is_stable_counting_sort():
