@@ -2,10 +2,12 @@
 """Decode-step benchmark of the ODS hot path on one MI355X.
 
 One step = one decode step of the workload's block (for the default workload,
-one 8B-shaped dense layer: the attention stage, ops [0, 6), then the FFN stage,
-ops [6, 10)) over the whole batch, with every input already resident in HBM.
-Three independent copies of the weights and KV pools are used in rotation so
-that no step finds the previous step's bytes in the 256 MB last-level cache.
+one 8B-shaped dense layer at batch 256 with every context 8192 tokens: the
+attention stage, ops [0, 6), then the FFN stage, ops [6, 10)) over the whole
+batch, with every input already resident in HBM. A step that moves less than
+2 GB uses three independent copies of the weights and KV pools in rotation, so
+that no step finds the previous step's bytes in the 256 MB last-level cache
+(the default step reads 8.7 GB of KV and weights and needs no copies).
 
 Prints one JSON line: whole-step decode tokens/s, per-stage tokens/s with their
 fraction of the HBM / MFMA roofline, the roofline of the dominant operator
@@ -104,7 +106,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="dense8b_b64")
+    ap.add_argument("--workload", default="dense8b_b256_ctx8k")
     ap.add_argument("--copies", type=int, default=0, help="weight/KV copies in rotation (0: auto)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--weights", choices=("tiled", "rows"), default="tiled",
@@ -114,6 +116,9 @@ def parse():
                     help="sliding-window layers keep their KV in a window-only page ring "
                          "(ceil(window / 16) + 1 pages per sequence) instead of full page tables")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work to time")
+    ap.add_argument("--cpu-rows", type=int, default=8,
+                    help="sequences of the batch the CPU oracle baseline decodes (spread over the batch, "
+                         "longest and shortest context included)")
     ap.add_argument("--ffn-sweep", action="store_true",
                     help="instead of the decode step, time the dense FFN stage alone over batch sizes "
                          "64..2048 to show where the GEMMs turn from HBM- to MFMA-bound")
@@ -187,48 +192,75 @@ def measured_traffic(workload):
 
 # ----------------------------------------------------------------------------- CPU baseline
 
-def cpu_baseline(w, copy0, budget_s):
-    """Time the float64 oracle on the host over whole-batch decode steps of the
-    same workload (first weight/KV copy), repeated until ~budget_s."""
+def cpu_baseline(w, copy0, budget_s, n_rows):
+    """Time the float64 oracle on the host, stage by stage, over decode steps
+    of a bounded sample of the workload's sequences (first weight/KV copy),
+    repeated until ~budget_s of oracle time. The attention stage (a Python
+    loop over rows and heads of small numpy calls) runs with numpy's BLAS
+    limited to one thread, which measured as fast as the full pool; the FFN
+    stage (large matrix products) with the whole BLAS pool. `cores` is the
+    largest thread count a stage used; each stage also reports its own
+    threads and its CPU-seconds per wall-second."""
     import oracle as O
     import torch
-    from threadpoolctl import threadpool_info
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     def f64(t):
-        return t.detach().float().cpu().numpy().astype(np.float64)
+        return t.detach().double().cpu().numpy()
 
     cfgs = list(w.layers)
-    n_rows = w.batch
-    rows = np.arange(n_rows)
-    # inputs of the sampled rows (their pages only), converted once, not timed
-    ctx = copy0["ctx"][rows]
+    ctx_all = copy0["ctx"]
+    rows = set(np.linspace(0, w.batch - 1, n_rows).round().astype(int).tolist())
+    rows |= {int(np.argmax(ctx_all)), int(np.argmin(ctx_all))}
+    rows = np.array(sorted(rows))
+    # inputs of the sampled rows (their pages only; a sliding-window layer only
+    # its window's pages), converted once, not timed
+    ctx = ctx_all[rows]
     pt = copy0["page_table"][rows]
-    n_pages = [-(-int(c) // 16) for c in ctx]
-    pages = np.concatenate([pt[i, :n] for i, n in enumerate(n_pages)])
-    sub = np.full((len(rows), pt.shape[1]), -1, dtype=np.int32)
-    off = 0
-    for i, n in enumerate(n_pages):
-        sub[i, :n] = np.arange(off, off + n)
-        off += n
-    idx = torch.from_numpy(pages.astype(np.int64)).cuda()
+    tables, pools0 = [], []
+    for cfg, pool in zip(cfgs, copy0["pools"]):
+        table = np.full(pt.shape, -1, dtype=np.int32)
+        pages, off = [], 0
+        for i, c in enumerate(ctx):
+            n = -(-int(c) // 16)
+            p0 = max(0, int(c) - cfg.window) // 16 if cfg.window > 0 else 0
+            pages.append(pt[i, p0:n])
+            table[i, p0:n] = np.arange(off, off + n - p0)
+            off += n - p0
+        idx = torch.from_numpy(np.concatenate(pages).astype(np.int64)).cuda()
+        pools0.append(f64(pool.index_select(0, idx)))
+        tables.append(table)
     weights = [{k: f64(v) for k, v in wl.items()} for wl in copy0["weights"]]
-    pools0 = [f64(p.index_select(0, idx)) for p in copy0["pools"]]
     x = f64(copy0["x"][torch.from_numpy(rows).cuda()])
-    n_ops = sum(14 if c.n_experts else 10 for c in cfgs)
-    done, t_total, reps = 0, 0.0, 0
+    offs = np.cumsum([0] + [14 if c.n_experts else 10 for c in cfgs])
+    blas = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    threads = {"attn": 1, "ffn": int(blas)}
+    wall = {"attn": 0.0, "ffn": 0.0}
+    cpu = {"attn": 0.0, "ffn": 0.0}
+    reps = 0
     while True:
         pools = [p.copy() for p in pools0]
-        t0 = time.perf_counter()
-        O.run_ops(cfgs, weights, pools, sub, ctx, {"resid": x.copy()}, 0, n_ops)
-        t_total += time.perf_counter() - t0
-        done += len(rows)
+        live = {"resid": x.copy()}
+        for l in range(len(cfgs)):
+            for stage, a, b in (("attn", offs[l], offs[l] + 6), ("ffn", offs[l] + 6, offs[l + 1])):
+                with threadpool_limits(threads[stage]):
+                    c0, t0 = time.process_time(), time.perf_counter()
+                    live = O.run_ops(cfgs, weights, pools, tables, ctx, live, int(a), int(b))
+                    wall[stage] += time.perf_counter() - t0
+                    cpu[stage] += time.process_time() - c0
         reps += 1
-        if t_total >= budget_s * 0.5 or reps >= 50:
+        if wall["attn"] + wall["ffn"] >= budget_s or reps >= 50:
             break
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return {"value": done / t_total, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{reps} whole-batch decode steps ({len(rows)} sequences, all ops) of the "
-                      f"{w.name} workload, float64 numpy oracle, {t_total:.1f} s"}
+    tokens = reps * len(rows)
+    t = wall["attn"] + wall["ffn"]
+    stages = {k: {"tokens_per_s": tokens / wall[k], "seconds": wall[k], "threads": threads[k],
+                  "cpu_seconds_per_wall_second": cpu[k] / wall[k]} for k in wall}
+    return {"value": tokens / t, "unit": "tokens/s", "cores": max(threads.values()),
+            "kind": "oracle", "host_cpus": os.cpu_count(), "stages": stages,
+            "sample": f"{reps} decode steps of {len(rows)} of the {w.batch} sequences of the {w.name} workload "
+                      f"(spread over the batch, longest and shortest context included; every layer, attention "
+                      f"stage on 1 thread and FFN stage on {threads['ffn']} BLAS threads timed separately), "
+                      f"float64 numpy oracle, {t:.1f} s"}
 
 
 # ----------------------------------------------------------------------------- main
@@ -491,6 +523,18 @@ def main():
 
     # per-stage and attn_core durations from the in-loop events
     core_ms, attn_ms, ffn_ms = [], [], []
+    per_layer = [{"attn": [], "core": [], "ffn": []} for _ in range(n_layers)]
+    for start, evs in per_step_events:
+        prev, layer_start = start, start
+        for (l, tag, ev) in evs:
+            if tag == "core":
+                per_layer[l]["core"].append(prev.elapsed_time(ev))
+            elif tag == "attn":
+                per_layer[l]["attn"].append(layer_start.elapsed_time(ev))
+            elif tag == "ffn":
+                per_layer[l]["ffn"].append(prev.elapsed_time(ev))
+                layer_start = ev
+            prev = ev
     for start, evs in per_step_events:
         prev = start
         a_ms = f_ms = c_ms = 0.0
@@ -523,6 +567,17 @@ def main():
                 "mfma_TFLOPs": flops / t / 1e12, "mfma_frac": flops / t / MFMA_BF16_PEAK,
                 "roofline_us": max(nbytes / HBM_PEAK, flops / MFMA_BF16_PEAK) * 1e6}
 
+    layers_out = []
+    for l, cfg in enumerate(w.layers):
+        med = {k: float(np.median(v)) * 1e-3 for k, v in per_layer[l].items()}
+        a = acct[l]
+        layers_out.append({
+            "layer": l, "window": cfg.window, "attention": "sliding window" if cfg.window else "full",
+            "attn_stage_us": med["attn"] * 1e6, "attn_stage_hbm_frac": a["attn_bytes"] / med["attn"] / HBM_PEAK,
+            "attn_core_us": med["core"] * 1e6, "attn_core_bytes": a["attn_core_bytes"],
+            "attn_core_hbm_frac": a["attn_core_bytes"] / med["core"] / HBM_PEAK,
+            "ffn_stage_us": med["ffn"] * 1e6, "ffn_stage_mfma_frac": a["ffn_flops"] / med["ffn"] / MFMA_BF16_PEAK,
+            "ffn_stage_hbm_frac": a["ffn_bytes"] / med["ffn"] / HBM_PEAK})
     achieved = core_bytes / t_core
     traffic = measured_traffic(w.name)
     result = {
@@ -546,6 +601,7 @@ def main():
                    "kv_ring_pages": ring_pages, "kv_pool_bytes_per_layer": kv_pool_bytes,
                    "kv_pool_bytes_total": int(sum(kv_pool_bytes))},
         "stages": {"attn": stage(t_attn, attn_bytes, attn_flops), "ffn": stage(t_ffn, ffn_bytes, ffn_flops)},
+        "layers": layers_out,
         "handoff": {"cut": "after local op 5 (attention stage | FFN stage)",
                     "bytes_per_token": handoff_bytes_per_token(w.layers[0])["5"],
                     "bytes_per_token_by_cut": handoff_bytes_per_token(w.layers[0])},
@@ -556,7 +612,7 @@ def main():
                      "algorithmic_bytes_per_launch": core_bytes, "avg_launch_us": t_core * 1e6},
     }
     if not args.no_cpu_baseline and not ring_pages:  # the oracle baseline reads the full page tables
-        result["cpu_baseline"] = cpu_baseline(w, sets[0], args.cpu_budget)
+        result["cpu_baseline"] = cpu_baseline(w, sets[0], args.cpu_budget, args.cpu_rows)
     print(json.dumps(result), flush=True)
 
 
