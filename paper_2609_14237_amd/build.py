@@ -18,6 +18,13 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall", "-Wno-u
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", os.path.join(ROOT, "include")]
 SOURCES = ["k_gemm.hip", "k_gemm_stream.hip", "k_attn.hip", "k_elem.hip", "k_moe.hip", "ods_api.cpp"]
+# The HIP-free host part (validation, allocator, sizing, planning) builds with
+# the host compiler alone; tests/test_host_sanitize.py builds it again under
+# the CPU sanitizers.
+HOST_SOURCES = ["ods_host.cpp"]
+HOST_CXX = os.environ.get("CXX", "g++")
+HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I", "/opt/rocm/include",
+              "-I", os.path.join(ROOT, "include")]
 # Per-file flags: the weight-streaming GEMM keeps its MFMA accumulators in
 # VGPRs (with AGPR results the allocator copies them around the K loop).
 EXTRA = {"k_gemm_stream.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
@@ -32,10 +39,19 @@ def _compile(src: str) -> str:
     return obj
 
 
+def _compile_host(src: str) -> str:
+    obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
+    cmd = [HOST_CXX, *HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"{HOST_CXX} failed for {src}:\n{r.stdout}\n{r.stderr}")
+    return obj
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES) + len(HOST_SOURCES))) as ex:
+        objs = list(ex.map(_compile, SOURCES)) + list(ex.map(_compile_host, HOST_SOURCES))
     tmp = OUT + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)

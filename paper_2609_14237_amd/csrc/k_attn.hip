@@ -426,45 +426,6 @@ int num_cus() {
   return n;
 }
 
-// Grid of the attention kernel: one 4-wave block per compute unit, fewer when
-// the batch cannot fill them with ranges of at least 8 pages. Fewer waves in
-// flight stream the pool faster: measured on one MI355X, B = 64 x U[512, 4096]
-// 122.7 -> 115.6 us, B = 256 x 8192 1444 -> 1376 us, MoE B = 512 1593 ->
-// 1563 us from three blocks per unit to one (two was in between). The kernel
-// is built for at most two waves per SIMD (256 VGPRs), which leaves its 170
-// registers unspilled.
-int attn_grid(int B, int n_kv, int span) {
-  const int64_t max_units = (int64_t)B * n_kv * span;
-  return (int)std::max<int64_t>(1, std::min<int64_t>(num_cus(), (max_units + 31) / 32));
-}
-
-int attn_span(int max_pages, int window) {
-  int span = max_pages;
-  if (window > 0) span = std::min(max_pages, (window + kPage - 1) / kPage + 1);
-  return std::max(span, 1);
-}
-
-AttnPlan attn_plan(int B, int n_kv, int D, int max_pages, int window, int split_pages_req) {
-  (void)D;
-  const int span = attn_span(max_pages, window);
-  AttnPlan plan;
-  plan.seg_pages = split_pages_req;
-  plan.grid = attn_grid(B, n_kv, span);
-  // Records r + seq with r a range index: ranges <= waves when S is chosen
-  // from the total, else <= ceil(max units / S).
-  const int64_t seqs = (int64_t)B * n_kv;
-  const int64_t ranges = split_pages_req > 0 ? (seqs * span + split_pages_req - 1) / split_pages_req
-                                             : (int64_t)plan.grid * 4;
-  plan.records = ranges + seqs;
-  plan.units_ok = seqs * span < (int64_t)1 << 30;
-  return plan;
-}
-
-size_t attn_ws_bytes(int B, int n_q, int n_kv, int D, const AttnPlan &plan) {
-  const size_t group = n_q / n_kv;
-  return (size_t)B * n_kv * sizeof(int2) + (size_t)plan.records * group * (D + 2) * sizeof(float);
-}
-
 hipError_t launch_attention(const uint16_t *qkv, int B, int n_q, int n_kv, int D, int window,
                             const int32_t *ctx_lens, const int32_t *page_table, int max_pages, int ring,
                             const uint16_t *pool, int64_t pool_pages, const AttnPlan &plan, float *ws,

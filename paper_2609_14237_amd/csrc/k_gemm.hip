@@ -402,7 +402,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs p) {
   *(u32x2 *)c = o;
 }
 
-constexpr int kBM = 64, kBK = 128;
+constexpr int kBM = kDecodeBM, kBK = kDecodeBK;
 
 size_t lds_bytes(int BM, int BN, int BK, bool silu) { return (size_t)2 * (BM + (silu ? 2 : 1) * BN) * (BK + 8) * 2; }
 
@@ -424,22 +424,6 @@ hipError_t launch_big(const GemmArgs &a, dim3 grid, hipStream_t s) {
   if (hipError_t e = ensure_lds_limit((const void *)kern, lds, lds_set); e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, grid, dim3(512), lds, s, a);
   return hipGetLastError();
-}
-
-// Large-M tiles pay off when the output is wide enough to fill 128-column
-// tiles; a narrow output (the router's expert logits) stays on 64-row tiles.
-bool use_big(int M, int N) { return M > kBM && N > 128; }
-
-// Output tile width: 32 columns for narrow outputs (more blocks), 64 otherwise.
-// SiLU-gated outputs count gate and up rows, so their tile is half as wide.
-// A long-K narrow output (K >= 2N, the down projection) takes 64 columns: every
-// block re-reads the activation rows of its K range, and at 32 columns those
-// re-reads cost twice the weight bytes (down at M = 64: 38.4 -> 31.3 us with
-// 8-way split-K restoring the block count).
-bool long_k(int N, int K, int epi) { return epi != EPI_SILU && N > 128 && K >= 2 * N; }
-int tile_n(int N, int K, int epi) {
-  if (long_k(N, K, epi)) return 64;
-  return (epi == EPI_SILU ? 2 * N : N) <= 8192 ? 32 : (epi == EPI_SILU ? 32 : 64);
 }
 
 template <int EPI>
@@ -488,41 +472,6 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
 }
 
 }  // namespace
-
-int gemm_splits(int M, int N, int K, int epi, bool b_tiled) {
-  if (b_tiled || gemm_use_stream(M, N, K, epi)) return gemm_stream_splits(M, N, K, epi);
-  if (N % 4 != 0) return 1;  // the reduce works on 4-column groups
-  if (use_big(M, N)) {
-    // Large-M tiles: one 512-thread block per compute unit; split K (up to 8
-    // ways, at least 8 steps of 64 per block) until ~192 blocks are in flight.
-    const int bm = M > 128 ? 256 : 128, bn = epi == EPI_SILU ? 64 : 128;
-    const int tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
-    const int steps = (K + 63) / 64;
-    int s = 1;
-    while (tiles * s < 192 && s < 8 && steps / (s * 2) >= 8) s *= 2;
-    return s;
-  }
-  const int bn = tile_n(N, K, epi);
-  const int tiles = ((M + kBM - 1) / kBM) * ((N + bn - 1) / bn);
-  const int steps = (K + kBK - 1) / kBK;
-  int s = 1;
-  // Too few tiles leaves HBM idle: split K up to 4 ways (8 for long K) until
-  // there are about two blocks per compute unit, keeping at least 8 K steps
-  // per block. The SiLU-gated GEMM is wide enough at decode batches and skips
-  // the extra pass. A narrow output has few tiles at any batch: split it up to
-  // 16 ways, down to 2 K steps per block.
-  const int want = epi == EPI_SILU ? 256 : 512;
-  const bool narrow = N <= 128;
-  const int max_s = narrow ? 16 : long_k(N, K, epi) ? 8 : 4, min_steps = narrow ? 2 : 8;
-  while (tiles * s < want && s < max_s && steps / (s * 2) >= min_steps) s *= 2;
-  return s;
-}
-
-size_t gemm_partial_bytes(int M, int N, int K, int epi, bool b_tiled) {
-  const int s = gemm_splits(M, N, K, epi, b_tiled);
-  if (s <= 1) return 0;
-  return (size_t)s * M * N * (epi == EPI_SILU ? 2 : 1) * sizeof(float);
-}
 
 hipError_t launch_splitk_reduce(const GemmArgs &a, hipStream_t s) {
   const int64_t quads = (int64_t)a.M * a.N / 4;

@@ -377,11 +377,6 @@ __global__ __launch_bounds__(256) void tile_weight_kernel(const uint16_t *__rest
 
 }  // namespace
 
-int64_t tiled_weight_elems(int out, int in, bool gated, int groups) {
-  const int64_t tiles = gated ? (out + 63) / 64 : (out + 127) / 128;
-  return (int64_t)groups * tiles * (in / 64) * (128 * 64);
-}
-
 hipError_t launch_tile_weight(const uint16_t *src, uint16_t *dst, int out, int in, bool gated, int groups,
                               hipStream_t s) {
   const int n_tiles = gated ? (out + 63) / 64 : (out + 127) / 128;
@@ -390,27 +385,6 @@ hipError_t launch_tile_weight(const uint16_t *src, uint16_t *dst, int out, int i
   hipLaunchKernelGGL(tile_weight_kernel, dim3((unsigned)blocks), dim3(256), 0, s, src, dst, out, in, gated ? 1 : 0,
                      n_tiles, n_chunks);
   return hipGetLastError();
-}
-
-// Dense GEMMs past 128 rows, and those of 33 to 64 rows except the SiLU-gated
-// one (64-row tiles: at 64 rows qkv 20.2 -> 18.0 us, o_proj 16.4 -> 15.9 us and
-// down 31.8 -> 29.2 us on the 8B-shaped layer, gate_up level at 53 us and
-// slower below 48 rows; at 32 rows and fewer the gains are under 1 us).
-bool gemm_use_stream(int M, int N, int K, int epi) {
-  if (N <= 128 || K % 64 != 0) return false;
-  return M > 128 || (M > 32 && M <= 64 && epi != EPI_SILU);
-}
-
-// Split K (1, 2, 4 or 8 ways, at least 8 steps per split) until about 192
-// blocks are in flight; the reduce works on 4-column groups.
-int gemm_stream_splits(int M, int N, int K, int epi) {
-  if (N % 4 != 0) return 1;
-  const int bn = epi == EPI_SILU ? 64 : 128;
-  const int tiles = ((M + 255) / 256) * ((N + bn - 1) / bn);
-  const int steps = K / 64;
-  int s = 1;
-  while (tiles * s < 192 && s < 8 && steps / (s * 2) >= 8) s *= 2;
-  return s;
 }
 
 hipError_t launch_gemm_stream(const GemmArgs &a, hipStream_t s) {
