@@ -141,8 +141,8 @@ typedef struct {
  *
  * Window-only page ring (ring_pages > 0). A sliding-window layer only ever
  * reads the most recent `window` tokens, so its KV pages can live in a ring
- * (the paper's hybrid-architecture discussion: efficient attention operators
- * access a bounded window, Section 3): with ring_pages = R > 0, every layer of
+ * (a sliding-window layer reads at most its window of KV; Section 3, hybrid
+ * architectures): with ring_pages = R > 0, every layer of
  * the call with window > 0 maps token position t of sequence b to page
  * ring_table[b][(t / 16) % R], slot t % 16, of its own kv_pool, and its
  * contexts are not clamped to max_pages * 16. Full-attention layers keep
