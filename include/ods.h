@@ -46,7 +46,8 @@
  *
  * Ownership and errors. The caller owns all memory and the stream. The library
  * never allocates, frees, synchronises, or changes the current device, and
- * keeps no state between calls. Every argument is checked on the host before
+ * keeps no state between calls (apart from the static workspace array of
+ * ods_run_partition_scratch). Every argument is checked on the host before
  * anything is enqueued: a non-OK status means nothing was enqueued, except
  * ODS_EHIP, which reports a launch failure after earlier kernels of the same
  * call were enqueued. Device faults surface at the caller's synchronisation.
