@@ -25,8 +25,12 @@
 //                           the page, so lane l reads 8 contiguous bytes, and P
 //                           is already in the B-operand layout of S^T.
 // The accumulator O^T keeps head l%16 in lane l, so the softmax rescale never
-// leaves the lane. Two pages are in flight per wave (register ping-pong), and
-// the page ids of the next 64 pages load while the current 64 are streamed.
+// leaves the lane. K and V reach registers through LDS: each wave streams its
+// pages with direct-to-LDS loads into a ring of two page slots of its own and
+// reads a slot into registers once its loads have landed, so the page in
+// flight costs no registers. The group's q rows are read once per segment,
+// not once per page. The page ids of the next 64 pages load while the current
+// 64 are streamed.
 #include <math.h>
 
 #include <algorithm>
@@ -38,6 +42,11 @@ namespace ods {
 
 namespace {
 
+constexpr int kNonTemporal = 2;  // cache-policy operand of the direct-to-LDS load: nt
+// Largest dynamic LDS a launch asks for: the per-sequence arrays at the batch
+// limit plus two K+V page slots for each of the four waves at D = 128.
+constexpr size_t kMaxAttnLds = ((2 * (size_t)kMaxAttnBatch + 1) * sizeof(int) + 15) / 16 * 16 + 4 * 2 * 2 * 16 * 128 * 2;
+
 template <int D>
 struct PageRegs {
   u32x4 k[D / 32];  // K rows: lane l holds K[t = l%16][kk*32 + (l/16)*8 .. +8]
@@ -47,6 +56,12 @@ struct PageRegs {
   int seq;          // b * n_kv + g, -1 for a padding slot past the range (uniform)
   int lo, p;        // attended token positions [lo, p] of the sequence (uniform)
   bool ok;          // page id inside the pool (uniform)
+};
+
+// Uniform description of a page whose K / V loads are in flight in an LDS slot.
+struct PageMeta {
+  int pg, seq, lo, p;  // as in PageRegs
+  bool ok;
 };
 
 // Attended window of a sequence from its (clamped) context: token positions
@@ -114,6 +129,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     if (tid == 255) s_pre[B] = run * n_kv;
     __syncthreads();
   }
+  // This wave's LDS page slots, after the per-sequence arrays: K block, then V block.
+  constexpr int kSlots = 2;
+  constexpr int SLOT = 2 * kPage * D * 2;
+  constexpr int LPP = 2 * (kPage * D * 2 / 1024);  // 16-byte direct-to-LDS loads per page and lane
+  uint8_t *const slots = (uint8_t *)smem_i + (((2 * B + 1) * 4 + 15) & ~15) + wave * kSlots * SLOT;
   const int total = __builtin_amdgcn_readfirstlane(s_pre[B]);
   const int n_waves = gridDim.x * 4;
   const int S = seg_pages > 0 ? seg_pages : max(8, (total + n_waves - 1) / n_waves);
@@ -166,10 +186,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     int it = 0;  // range page index of the next issue
     int ids_cur = gather_ids(0), ids_nxt = gather_ids(64);
 
-    // Issue the loads of the cursor's page into R and advance the cursor. Past
-    // the range the slot re-reads a valid page and is marked as padding, so the
-    // loads stay unconditional and the compiler can count them in flight.
-    auto issue = [&](PageRegs<D> &R) {
+    // Issue the loads of the cursor's page into LDS slot `slot`, describe it
+    // in R and advance the cursor. Past the range the slot re-reads a valid
+    // page and is marked as padding, so every issue makes the same loads and
+    // the waits can count them.
+    auto issue = [&](PageMeta &R, int slot) {
       if (it > 0 && (it & 63) == 0) {
         ids_cur = ids_nxt;
         ids_nxt = gather_ids(it + 64);
@@ -182,18 +203,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       R.p = ip;
       R.ok = live && (unsigned)page < (unsigned long long)pool_pages;
       const uint16_t *kb = pool + (int64_t)ig * BLK + (int64_t)(R.ok ? page : 0) * page_stride;
-      // K/V bytes are read once per launch: non-temporal loads (the nt cache
-      // policy) stream them past the caches instead of evicting the q rows,
-      // page ids and records the kernel does reuse (B = 64: 115 -> 103 us).
+      uint8_t *const dst = slots + slot * SLOT;
+      // A direct-to-LDS load writes lane l's 16 bytes at byte 16 l of its
+      // destination. K: lane l fetches the 16 bytes it will read as its MFMA
+      // fragment (K[t = l % 16][kk * 32 + (l / 16) * 8 ..]), so its read-back is
+      // at 16 l, conflict-free. V: the dim-major block is copied verbatim and
+      // lane l reads its 8 bytes (dim nb * 16 + l % 16, slots (l / 16) * 4 ..)
+      // at (nb * 16 + l % 16) * 32 + (l / 16) * 8. K/V bytes are read once per
+      // launch: the loads carry the non-temporal cache policy.
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk)
-        R.k[kk] = __builtin_nontemporal_load((const u32x4 *)(kb + hl * D + kk * 32 + rq * 8));
+        __builtin_amdgcn_global_load_lds((const void *)(kb + hl * D + kk * 32 + rq * 8),
+                                         (__attribute__((address_space(3))) void *)(dst + kk * 1024), 16, 0,
+                                         kNonTemporal);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        R.v[nb] = __builtin_nontemporal_load((const u32x2 *)(kb + v_off + (nb * 16 + hl) * kPage + rq * 4));
-      const uint16_t *qp = qkv + (int64_t)ib * row_elems + (int64_t)(ig * group + (head_ok ? hl : 0)) * D;
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) R.q[kk] = *(const u32x4 *)(qp + kk * 32 + rq * 8);
+      for (int j = 0; j < KK; ++j)
+        __builtin_amdgcn_global_load_lds((const void *)((const uint8_t *)(kb + v_off) + j * 1024 + lane * 16),
+                                         (__attribute__((address_space(3))) void *)(dst + kPage * D * 2 + j * 1024),
+                                         16, 0, kNonTemporal);
       if (live) {
         ++it;
         if (++ipage == in_b) {
@@ -308,17 +335,54 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
     };
 
-    // Two pages in flight: while one is consumed the next is loading; the
-    // stream runs across segment boundaries without draining.
-    PageRegs<D> R0, R1;
-    issue(R0);
-    issue(R1);
-    for (int t = 0; t < n_w; t += 2) {
-      consume(R0);
-      issue(R0);
-      if (t + 1 < n_w) consume(R1);
-      issue(R1);
+    // Two pages in flight through the wave's LDS slots: while one is consumed
+    // the next is loading; the stream runs across segment boundaries without
+    // draining. A wave's loads complete in order, so slot s has landed once
+    // only the other slot's LPP loads are outstanding. The q rows of a segment
+    // are loaded when its first page is consumed, and that path alone waits
+    // for every load.
+    PageMeta ms[kSlots];
+    u32x4 qreg[KK];
+    int q_seq = -1;
+#pragma unroll
+    for (int sl = 0; sl < kSlots; ++sl) issue(ms[sl], sl);
+    for (int t = 0; t < n_w; t += kSlots) {
+#pragma unroll
+      for (int sl = 0; sl < kSlots; ++sl) {
+        if (t + sl < n_w) {
+          asm volatile("s_waitcnt vmcnt(%0)" ::"n"((kSlots - 1) * LPP) : "memory");
+          PageRegs<D> R;
+          const uint8_t *src = slots + sl * SLOT;
+#pragma unroll
+          for (int kk = 0; kk < KK; ++kk) R.k[kk] = *(const u32x4 *)(src + kk * 1024 + lane * 16);
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            R.v[nb] = *(const u32x2 *)(src + kPage * D * 2 + (nb * 16 + hl) * 32 + rq * 8);
+          if (ms[sl].seq >= 0 && ms[sl].seq != q_seq) {
+            q_seq = ms[sl].seq;
+            const int qb = q_seq / n_kv, qg = q_seq % n_kv;
+            const uint16_t *qp = qkv + (int64_t)qb * row_elems + (int64_t)(qg * group + (head_ok ? hl : 0)) * D;
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) qreg[kk] = *(const u32x4 *)(qp + kk * 32 + rq * 8);
+            // vmcnt(0) on this path only (a builtin, so the compiler knows the q
+            // registers have landed and adds no wait on the common path)
+            __builtin_amdgcn_s_waitcnt(0x0F70);
+          }
+#pragma unroll
+          for (int kk = 0; kk < KK; ++kk) R.q[kk] = qreg[kk];
+          R.pg = ms[sl].pg;
+          R.seq = ms[sl].seq;
+          R.lo = ms[sl].lo;
+          R.p = ms[sl].p;
+          R.ok = ms[sl].ok;
+          consume(R);
+        }
+        issue(ms[sl], sl);
+      }
     }
+    // No load may still be writing the slots when the next range reuses them
+    // or the wave retires.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     finish();
   }
 }
@@ -435,10 +499,12 @@ hipError_t launch_attention(const uint16_t *qkv, int B, int n_q, int n_kv, int D
   float *ws_acc = ws;  // [records][group][D], 16-byte aligned rows
   float *ws_ml = ws_acc + (size_t)plan.records * group * D;
   int2 *ws_meta = (int2 *)(ws_ml + (size_t)plan.records * group * 2);
-  const size_t lds = (2 * (size_t)B + 1) * sizeof(int);
+  // per-sequence arrays, then two K+V page slots per wave (64 KB at D = 128)
+  const size_t lds = (((2 * (size_t)B + 1) * sizeof(int) + 15) & ~(size_t)15) + (size_t)4 * 2 * 2 * kPage * D * 2;
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
   const dim3 mgrid((unsigned)(((int64_t)B * n_q + 3) / 4));
-  auto go = [&](auto kflat, auto kmerge) {
+  auto go = [&](auto kflat, auto kmerge, std::atomic<uint64_t> &lds_set) {
+    if (hipError_t e = ensure_lds_limit((const void *)kflat, kMaxAttnLds, lds_set); e != hipSuccess) return e;
     hipLaunchKernelGGL(kflat, dim3(plan.grid), dim3(256), lds, s, qkv, n_q, n_kv, window, ctx_lens, page_table,
                        max_pages, ring, pool, pool_pages, plan.seg_pages, scale_log2, ws_acc, ws_ml, ws_meta, o, B);
     hipError_t e = hipGetLastError();
@@ -446,8 +512,9 @@ hipError_t launch_attention(const uint16_t *qkv, int B, int n_q, int n_kv, int D
     hipLaunchKernelGGL(kmerge, mgrid, dim3(256), 0, s, ws_acc, ws_ml, ws_meta, n_q, n_kv, ctx_lens, o, B);
     return hipGetLastError();
   };
-  if (D == 128) return go(attn_flat_kernel<128>, attn_merge_kernel<128>);
-  return go(attn_flat_kernel<64>, attn_merge_kernel<64>);
+  static std::atomic<uint64_t> lds_set_128{0}, lds_set_64{0};  // devices whose limit each kernel already raised
+  if (D == 128) return go(attn_flat_kernel<128>, attn_merge_kernel<128>, lds_set_128);
+  return go(attn_flat_kernel<64>, attn_merge_kernel<64>, lds_set_64);
 }
 
 }  // namespace ods
