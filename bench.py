@@ -116,6 +116,8 @@ def parse():
                     help="sliding-window layers keep their KV in a window-only page ring "
                          "(ceil(window / 16) + 1 pages per sequence) instead of full page tables")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work to time")
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="BLAS threads for the CPU baseline's FFN stage (0: the whole pool; 1: everything single-threaded)")
     ap.add_argument("--cpu-rows", type=int, default=8,
                     help="sequences of the batch the CPU oracle baseline decodes (spread over the batch, "
                          "longest and shortest context included)")
@@ -192,13 +194,14 @@ def measured_traffic(workload):
 
 # ----------------------------------------------------------------------------- CPU baseline
 
-def cpu_baseline(w, copy0, budget_s, n_rows):
+def cpu_baseline(w, copy0, budget_s, n_rows, ffn_threads=0):
     """Time the float64 oracle on the host, stage by stage, over decode steps
     of a bounded sample of the workload's sequences (first weight/KV copy),
     repeated until ~budget_s of oracle time. The attention stage (a Python
     loop over rows and heads of small numpy calls) runs with numpy's BLAS
     limited to one thread, which measured as fast as the full pool; the FFN
-    stage (large matrix products) with the whole BLAS pool. `cores` is the
+    stage (large matrix products) with the whole BLAS pool, or with
+    `ffn_threads` threads when that is positive. `cores` is the
     largest thread count a stage used; each stage also reports its own
     threads, the CPU-seconds per wall-second of the thread that calls the
     oracle, and those of the whole process (every thread, the GPU runtime's
@@ -236,7 +239,7 @@ def cpu_baseline(w, copy0, budget_s, n_rows):
     x = f64(copy0["x"][torch.from_numpy(rows).cuda()])
     offs = np.cumsum([0] + [14 if c.n_experts else 10 for c in cfgs])
     blas = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    threads = {"attn": 1, "ffn": int(blas)}
+    threads = {"attn": 1, "ffn": int(ffn_threads) if ffn_threads > 0 else int(blas)}
     wall = {"attn": 0.0, "ffn": 0.0}
     cpu = {"attn": 0.0, "ffn": 0.0}
     cpu_main = {"attn": 0.0, "ffn": 0.0}
@@ -617,7 +620,7 @@ def main():
                      "algorithmic_bytes_per_launch": core_bytes, "avg_launch_us": t_core * 1e6},
     }
     if not args.no_cpu_baseline and not ring_pages:  # the oracle baseline reads the full page tables
-        result["cpu_baseline"] = cpu_baseline(w, sets[0], args.cpu_budget, args.cpu_rows)
+        result["cpu_baseline"] = cpu_baseline(w, sets[0], args.cpu_budget, args.cpu_rows, args.cpu_threads)
     print(json.dumps(result), flush=True)
 
 
