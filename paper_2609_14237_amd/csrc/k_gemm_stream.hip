@@ -19,12 +19,14 @@ namespace {
 
 constexpr int kNonTemporal = 2;  // cache-policy operand of the direct-to-LDS load: nt
 
-// Two tile shapes (K % 64 == 0), both with two waves per SIMD and 128 rows of
-// B per block (SiLU: 64 gate + 64 up rows, each wave taking the gate and up
-// rows of the same output columns, so both halves of a column meet in one
+// Three tile shapes (K % 64 == 0), all with two waves per SIMD and 128 rows
+// of B per block (SiLU: 64 gate + 64 up rows, each wave taking the gate and
+// up rows of the same output columns, so both halves of a column meet in one
 // lane). MG = 4: 512 threads = 8 waves as 4 (M) x 2 (N) over a 256-row tile of
-// A, 144 KB of LDS, one block per CU. MG = 1: 256 threads = 4 waves as 1 x 4
-// over a 64-row tile, 72 KB, two blocks per CU. Wave (wm, wn) computes rows
+// A, three K steps of LDS (144 KB), one block per CU. MG = 2: 256 threads =
+// 4 waves as 2 x 2 over a 128-row tile, two K steps (64 KB), two blocks per
+// CU. MG = 1: 256 threads = 4 waves as 1 x 4 over a 64-row tile, three K
+// steps (72 KB), two blocks per CU. Wave (wm, wn) computes rows
 // [64 wm, 64 wm + 64) against its 128 / WN rows of B.
 //
 // Both operands go from global memory straight into LDS (direct-to-LDS loads:
@@ -33,29 +35,29 @@ constexpr int kNonTemporal = 2;  // cache-policy operand of the direct-to-LDS lo
 // 16 bytes in lane order; choosing which chunk each lane fetches XOR-swizzles
 // the chunks of each row by row index, so the MFMA fragment reads are
 // conflict-free. A rows land in an area per M group (shared by that group's
-// waves), B rows in an area all waves share; both are rings of three K steps,
-// filled two steps ahead. Two waves per SIMD matter: one wave per SIMD draws
-// about 25 B/clk from LDS, two about 50, and each wave reads 16 KB (MG = 4)
-// or 12 KB (MG = 1) of fragments per K step.
+// waves), B rows in an area all waves share; both are rings of NSLOT K steps,
+// filled NSLOT - 1 steps ahead. Two waves per SIMD matter: one wave per SIMD
+// draws about 25 B/clk from LDS, two about 50, and each wave reads 16 KB
+// (MG = 4, 2) or 12 KB (MG = 1) of fragments per K step.
 //
 // Synchronisation is explicit: the only vector-memory instructions in the
 // loop are these loads (one event type, completed in order), so at the top of
-// step t "vmcnt <= loads per step" means this wave's loads of step t have
-// landed, and the barrier that follows publishes every wave's share. The
-// loads of step t + 2 are issued after that barrier, into the slot step t - 1
-// read before it. The barrier is a bare s_barrier (the workgroup fence of
+// step t "vmcnt <= loads of NSLOT - 2 steps" means this wave's loads of step
+// t + 1 have landed, and the barrier that follows publishes every wave's
+// share. The loads of step t + NSLOT are issued after that barrier, into the
+// slot of step t, whose fragments are in registers by then. The barrier is a bare s_barrier (the workgroup fence of
 // __syncthreads would wait for every load in flight).
 //
 // Blocks are placed so that the compute units of one XCD share a K range
 // (split-K) and the M tiles of one weight slab run on one XCD at the same
 // time, so A slices and weight slabs are served by that XCD's L2. This file
 // is built with MFMA results in VGPRs, which keeps the accumulators in place.
-// MG = 64-row M groups per block (4 or 1, above).
-template <int MG, int EPI, bool PARTIAL>
+// MG = 64-row M groups per block (4, 2 or 1, above); NSLOT = K steps of LDS.
+template <int MG, int NSLOT, int EPI, bool PARTIAL>
 __global__ __launch_bounds__(MG == 4 ? 512 : 256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
-  constexpr int BK = 64, NSLOT = 3, BNR = 128;
-  constexpr int WN = MG == 4 ? 2 : 4, WAVES = MG * WN, BM = 64 * MG;
+  constexpr int BK = 64, BNR = 128;
+  constexpr int WN = MG == 1 ? 4 : 2, WAVES = MG * WN, BM = 64 * MG;
   constexpr bool SILU = EPI == EPI_SILU;
   constexpr int BN = SILU ? BNR / 2 : BNR;  // output columns per block
   constexpr int TN = 8 / WN;                // B fragments per wave and K half
@@ -169,7 +171,7 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
       constexpr bool NT = decltype(nt_c)::value;  // weight loads with the non-temporal policy
       constexpr int LW = LIVE ? LOADS : BL;  // loads per step of this wave
       auto issue = [&](int t, int slot) {
-        const int64_t k = (int64_t)min(t, last) * BK;
+        const int64_t k = (int64_t)t * BK;  // t <= last
         if (LIVE) {
 #pragma unroll
           for (int q = 0; q < AL; ++q)
@@ -180,7 +182,7 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
 #pragma unroll
         for (int q = 0; q < BL; ++q)
           __builtin_amdgcn_global_load_lds(
-              (const void *)(bptr[q] + min(t, last) * bstep),
+              (const void *)(bptr[q] + t * bstep),
               (__attribute__((address_space(3))) void *)(lds_b + slot * BSTAGE + (wave * BL + q) * 1024), 16, 0,
               NT ? kNonTemporal : 0);
       };
@@ -206,25 +208,26 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
       };
       // Step t runs its MFMAs on fragments read during step t - 1, reads the
       // fragments of step t + 1, and refills the slot of step t (free once its
-      // fragments are in registers) with the loads of step t + 3.
+      // fragments are in registers) with the loads of step t + NSLOT.
       issue(0, 0);
-      issue(1, 1);
-      issue(2, 2);
+#pragma unroll
+      for (int s = 1; s < NSLOT; ++s) issue(min(s, last), s);
       Frags f0, f1;
       __builtin_amdgcn_sched_barrier(0);
-      asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * LW) : "memory");
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"((NSLOT - 1) * LW) : "memory");
       __builtin_amdgcn_sched_barrier(0);
       if (LIVE) read_frags(f0, 0);
       int slot = 0;  // slot of step t
       auto step = [&](int t, const Frags &cur, Frags &nxt) {
-        // Loads of step t + 1 have landed once only those of step t + 2 are
-        // outstanding; lgkmcnt(0) retires this wave's reads of slot t (issued
-        // a step ago) before the barrier lets step t + 3 overwrite it.
+        // Loads of step t + 1 have landed once only those of the NSLOT - 2
+        // steps after it are outstanding; lgkmcnt(0) retires this wave's
+        // reads of slot t (issued a step ago) before the barrier lets step
+        // t + NSLOT overwrite it.
         __builtin_amdgcn_sched_barrier(0);
-        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LW) : "memory");
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"((NSLOT - 2) * LW) : "memory");
         __builtin_amdgcn_sched_barrier(0);
         const int s1 = slot == NSLOT - 1 ? 0 : slot + 1;
-        issue(t + 3, slot);
+        issue(min(t + NSLOT, last), slot);
         if (LIVE) {
           read_frags(nxt, s1);
           mma(cur);
@@ -255,7 +258,7 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
         step(t + 1, f1, f0);
       }
       if (t < nk) step(t, f0, f1);
-      // Nothing may still be writing the LDS slots when they are reused or the block retires.
+      // Nothing may still be reading the LDS slots when they are reused or the block retires.
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
     };
     if (nk > 0) {
@@ -313,39 +316,57 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
   }
 }
 
-template <int MG, int EPI, bool PARTIAL>
+template <int MG, int NSLOT, int EPI, bool PARTIAL>
 hipError_t launch_stream(const GemmArgs &a, hipStream_t s) {
   constexpr int BN = EPI == EPI_SILU ? 64 : 128;
   const int n_tiles = (a.N + BN - 1) / BN, m_tiles = (a.M + 64 * MG - 1) / (64 * MG);
   const int g = 8 / a.splits;  // splits is 1, 2, 4 or 8 (gemm_stream_splits)
   // dense: a 1-D grid placed on the XCDs; grouped: (N tile, group)
   const dim3 grid = a.group_off ? dim3(n_tiles, a.groups) : dim3(8 * m_tiles * ((n_tiles + g - 1) / g));
-  auto kern = gemm_stream_kernel<MG, EPI, PARTIAL>;
-  const size_t lds = (size_t)3 * 128 * 64 * 2 + MG * 3 * 64 * 64 * 2;  // 3 B slots + 3 A slots per M group
+  auto kern = gemm_stream_kernel<MG, NSLOT, EPI, PARTIAL>;
+  const size_t lds = (size_t)NSLOT * (128 * 64 * 2 + MG * 64 * 64 * 2);  // per slot: B tile + A tile per M group
   static std::atomic<uint64_t> lds_set{0};  // devices whose limit this kernel already raised
   if (hipError_t e = ensure_lds_limit((const void *)kern, lds, lds_set); e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, grid, dim3(MG == 4 ? 512 : 256), lds, s, a, n_tiles, m_tiles);
   return hipGetLastError();
 }
 
-// 64-row tiles (two blocks per CU) for batches of at most 64 rows and for
-// expert groups of at most 32 rows on average; 256-row tiles otherwise. With
-// about 64 rows per expert (the binomial spread puts half the experts above
-// 64) the 64-row tile needs a second pass over the weights for those experts:
-// 745 against 588 us for the expert GEMMs of a 512-token batch over 64
-// experts, top 8.
-bool gemm_stream_small_tile(const GemmArgs &a) {
-  if (a.group_off) return a.groups > 0 && a.M <= 32 * a.groups;
-  return a.M <= 64;
+// Tile shapes. Dense GEMMs: 64-row tiles (two blocks per CU) up to 64 rows,
+// 256-row tiles past that (at 96 and 128 rows the 256-row tile with idle
+// waves beats the 128-row one on every 8B-shaped GEMM, by 3-14 us). Grouped
+// (expert) GEMMs, by the average rows per group:
+//  - up to 32: 64-row tiles;
+//  - up to 96: 128-row tiles (two blocks per CU on a two-slot ring), which
+//    cover nearly every group in one pass while one block's start and end
+//    overlap the other's stream (top-8 of 64 experts, expert width 1536:
+//    down 182-185 -> 166 us and gate_up 287-295 -> 283 us at 64 rows per
+//    expert, 199 -> 175 and 312 -> 295 us at 96);
+//  - more: 256-row tiles (a 128-row tile would stream the weights of every
+//    group past 128 rows twice: at 128 rows per expert 237 against 209 us for
+//    down).
+enum StreamTile { TILE_64 = 0, TILE_128 = 1, TILE_256 = 2 };
+StreamTile gemm_stream_tile(const GemmArgs &a) {
+  if (a.group_off) {
+    if (a.groups <= 0 || a.M <= 32 * a.groups) return TILE_64;
+    return a.M <= 96 * a.groups ? TILE_128 : TILE_256;
+  }
+  return a.M <= 64 ? TILE_64 : TILE_256;
+}
+
+template <int MG, int NSLOT, int EPI>
+hipError_t launch_part(const GemmArgs &a, hipStream_t s) {
+  return a.splits > 1 ? launch_stream<MG, NSLOT, EPI, true>(a, s) : launch_stream<MG, NSLOT, EPI, false>(a, s);
 }
 
 template <int EPI>
 hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
-  const bool part = a.splits > 1;
-  const bool small = gemm_stream_small_tile(a);
-  hipError_t e = small ? (part ? launch_stream<1, EPI, true>(a, s) : launch_stream<1, EPI, false>(a, s))
-                       : (part ? launch_stream<4, EPI, true>(a, s) : launch_stream<4, EPI, false>(a, s));
-  if (e != hipSuccess || !part || a.defer_reduce) return e;
+  hipError_t e;
+  switch (gemm_stream_tile(a)) {
+    case TILE_64: e = launch_part<1, 3, EPI>(a, s); break;
+    case TILE_128: e = launch_part<2, 2, EPI>(a, s); break;
+    default: e = launch_part<4, 3, EPI>(a, s); break;
+  }
+  if (e != hipSuccess || a.splits <= 1 || a.defer_reduce) return e;
   return launch_splitk_reduce(a, s);
 }
 

@@ -17,6 +17,7 @@ import torch
 
 import oracle as O
 import workloads as W
+from workloads import gen
 from harness import Setup, assert_close, f64, oracle_run, report, routing_check
 
 pytestmark = pytest.mark.gpu
@@ -150,7 +151,7 @@ MOE_TILED = W.Workload("moe_tiled", (W.LayerCfg(hidden=512, n_q=8, n_kv=2, head_
 
 @pytest.mark.parametrize("batch", [48, 300])
 def test_moe_layer_on_tiled_weights(batch):
-    """Expert slabs in tile order (64-row tiles at 12 rows per expert, 256-row
+    """Expert slabs in tile order (64-row tiles at 12 rows per expert, 128-row
     tiles at 75), fused and unfused expert gate_up."""
     w = replace(MOE_TILED, batch=batch)
     cfg = w.layers[0]
@@ -176,3 +177,40 @@ def test_moe_layer_on_tiled_weights(batch):
         ref2 = oracle_run(fresh(inp), w.layers, 9, 14, live)
         assert_close(f"resid {cut}", f64(s.buf("resid", batch, cfg.hidden)), ref2["resid"])
     report(f"moe_tiled (batch {batch}) cuts: routing {summary}")
+
+
+@pytest.mark.parametrize("batch", [300, 450])
+@pytest.mark.parametrize("tiled", [False, True])
+def test_moe_skewed_groups(batch, tiled):
+    """The expert half [9, 14) on a routing where expert 0 takes 200 rows,
+    expert 1 none (an empty group) and the rest share the remainder. At batch
+    300 (75 rows per expert on average) the 128-row tile takes expert 0 in two
+    passes; at batch 450 (112.5) the 256-row tile takes it in one. Every
+    token's residual against the oracle on the same ids and weights."""
+    w = replace(MOE_TILED, batch=batch)
+    cfg = w.layers[0]
+    E, k, H = cfg.n_experts, cfg.top_k, cfg.hidden
+    say("skewed moe groups, batch", batch, "tiled", tiled)
+    s = Setup(w, seed=41, tiled=tiled)
+    ids = gen.expert_choices(batch, E - 2, k, 41) + 2
+    ids[:200, k - 1] = 0
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    rng = np.random.default_rng(41)
+    wts = rng.uniform(0.1, 1.0, (batch, k)).astype(np.float32)
+    wts /= wts.sum(axis=1, keepdims=True)
+    counts = np.bincount(ids.ravel(), minlength=E)
+    assert counts[0] == 200 and counts[1] == 0
+    hn = gen.live_tensor((batch, H), 41, 3, "cuda")
+    s.reset_resid()
+    s.buf("hn", batch, H).copy_(hn)
+    s.buf("topk_ids", batch, k).copy_(torch.from_numpy(ids))
+    s.buf("topk_w", batch, k).copy_(torch.from_numpy(wts))
+    s.run(9, 14)
+    torch.cuda.synchronize()
+    inp = s.oracle_inputs()
+    live = {"resid": inp["x"].copy(), "hn": f64(hn), "topk_ids": ids.astype(np.int64),
+            "topk_w": wts.astype(np.float64)}
+    ref = oracle_run(fresh(inp), w.layers, 9, 14, live)
+    e = assert_close(f"skewed resid batch {batch}", f64(s.buf("resid", batch, H)), ref["resid"])
+    report(f"moe skewed groups (batch {batch}, rows per expert {counts.min()}..{counts.max()}, "
+           f"{'tiled' if tiled else 'row-major'}): resid {e:.2e}")
