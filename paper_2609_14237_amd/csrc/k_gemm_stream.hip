@@ -18,6 +18,9 @@ namespace ods {
 namespace {
 
 constexpr int kNonTemporal = 2;  // cache-policy operand of the direct-to-LDS load: nt
+// Row pitch (floats) of the epilogue's LDS tile: 128 columns plus 4, so the
+// four rows one fragment write touches fall in different banks.
+constexpr int kStageRow = 132;
 
 // Three tile shapes (K % 64 == 0), all with two waves per SIMD and 128 rows
 // of B per block (SiLU: 64 gate + 64 up rows, each wave taking the gate and
@@ -106,6 +109,12 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
   // the 256-row tile, which measured slower with it (down at B = 256: 34 ->
   // 46 us).
   const bool b_once = (MG == 1 || p.splits == 1) && (p.group_off ? m_last - m_first <= BM : m_tiles == 1);
+  // The staged epilogue stores whole 16-byte chunks: every chunk must lie
+  // inside or outside the output columns, and start 16-byte aligned.
+  constexpr int CW_ = PARTIAL || EPI == EPI_F32 ? 4 : 8;
+  const int n_lim = !SILU && p.b_tiled && p.n_up > 0 ? p.n_up : p.N;
+  const bool vec = p.N % CW_ == 0 && n_lim % CW_ == 0 &&
+                   (PARTIAL ? ((uintptr_t)p.partial & 15) == 0 : p.ldc % CW_ == 0 && ((uintptr_t)p.C & 15) == 0);
 
   const int steps = p.K / BK;
   const int per = (steps + p.splits - 1) / p.splits;
@@ -270,12 +279,98 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
         else pipeline(std::false_type{}, std::false_type{});
       }
     }
-    if (!live) continue;
-
     // Epilogue: lane holds rows (lane >> 4) * 4 + e of column lane & 15 of each 16x16 tile.
     // A plain epilogue over gated tiles maps tile row rr to gate column
     // 64 nt + rr (rr < 64) or up column n_up + 64 nt + rr - 64.
     constexpr int TO = SILU ? TN / 2 : TN;  // output fragments (SiLU pairs gate jt with up jt + TO)
+    if (vec) {
+      // Staged through LDS (the drained slots): every live wave writes its
+      // fp32 results (SiLU: silu(gate) * up; SiLU partials: gate columns, then
+      // up columns) into a row-major tile, and the whole block stores it as
+      // 16-byte chunks, whole cache lines per row, instead of one 2- or 4-byte
+      // store per lane and value. The arithmetic is the scalar path's.
+      float *stage = (float *)smem;
+      if (live) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int jt = 0; jt < TO; ++jt) {
+            const int col = (SILU ? wn * (64 / WN) : wn * (128 / WN)) + jt * 16 + (lane & 15);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              float *row = stage + (wm * 64 + i * 16 + (lane >> 4) * 4 + e) * kStageRow;
+              if (SILU && !PARTIAL) {
+                row[col] = silu(acc[i][jt][e]) * acc[i][jt + TO][e];
+              } else {
+                row[col] = acc[i][jt][e];
+                if (SILU) row[64 + col] = acc[i][jt + TO][e];
+              }
+            }
+          }
+      }
+      __syncthreads();
+      constexpr bool F32OUT = PARTIAL || EPI == EPI_F32;
+      constexpr int CW = F32OUT ? 4 : 8;                      // outputs per 16-byte chunk
+      constexpr int CH = (SILU && !PARTIAL ? 64 : 128) / CW;  // chunks per tile row
+      const bool gated_cols = !SILU && p.b_tiled && p.n_up > 0;
+      const int rows = min(BM, m_last - m0);
+      for (int idx = tid; idx < rows * CH; idx += WAVES * 64) {
+        const int r = idx / CH, sc = (idx % CH) * CW, m = m0 + r;
+        const float *src = stage + r * kStageRow + sc;
+        int64_t dst;  // element offset of the chunk in C or in the partials
+        if (PARTIAL) {
+          const int64_t ncols = SILU ? 2 * (int64_t)p.N : p.N;
+          int n;
+          if (SILU) {
+            n = n0 + (sc & 63);
+            if (n >= p.N) continue;
+            if (sc >= 64) n += p.N;
+          } else if (gated_cols) {
+            const int c = nt * 64 + (sc & 63);
+            if (c >= p.n_up) continue;
+            n = sc < 64 ? c : p.n_up + c;
+          } else {
+            n = n0 + sc;
+            if (n >= p.N) continue;
+          }
+          dst = ((int64_t)split * p.M + m) * ncols + n;
+          *(f32x4 *)(p.partial + dst) = *(const f32x4 *)src;
+          continue;
+        }
+        int n;
+        if (gated_cols) {
+          const int c = nt * 64 + (sc & 63);
+          if (c >= p.n_up) continue;
+          n = sc < 64 ? c : p.n_up + c;
+        } else {
+          n = n0 + sc;
+          if (n >= p.N) continue;
+        }
+        dst = (int64_t)m * p.ldc + n;
+        if (EPI == EPI_F32) {
+          *(f32x4 *)((float *)p.C + dst) = *(const f32x4 *)src;
+          continue;
+        }
+        const f32x4 lo = *(const f32x4 *)src, hi = *(const f32x4 *)(src + 4);
+        float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        uint16_t *c = (uint16_t *)p.C + dst;
+        if (EPI == EPI_RESID) {
+          const u32x4 old = *(const u32x4 *)c;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            v[2 * q] += bf_lo(old[q]);
+            v[2 * q + 1] += bf_hi(old[q]);
+          }
+        }
+        u32x4 out;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) out[q] = pack2(v[2 * q], v[2 * q + 1]);
+        *(u32x4 *)c = out;
+      }
+      __syncthreads();  // the stage is read before the next tile's loads refill the slots
+      continue;
+    }
+    if (!live) continue;
     const bool gated_cols = !SILU && p.b_tiled && p.n_up > 0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -324,7 +419,8 @@ hipError_t launch_stream(const GemmArgs &a, hipStream_t s) {
   // dense: a 1-D grid placed on the XCDs; grouped: (N tile, group)
   const dim3 grid = a.group_off ? dim3(n_tiles, a.groups) : dim3(8 * m_tiles * ((n_tiles + g - 1) / g));
   auto kern = gemm_stream_kernel<MG, NSLOT, EPI, PARTIAL>;
-  const size_t lds = (size_t)NSLOT * (128 * 64 * 2 + MG * 64 * 64 * 2);  // per slot: B tile + A tile per M group
+  // per slot: B tile + A tile per M group; at least the epilogue's fp32 tile
+  const size_t lds = std::max<size_t>((size_t)NSLOT * (128 * 64 * 2 + MG * 64 * 64 * 2), (size_t)64 * MG * kStageRow * 4);
   static std::atomic<uint64_t> lds_set{0};  // devices whose limit this kernel already raised
   if (hipError_t e = ensure_lds_limit((const void *)kern, lds, lds_set); e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, grid, dim3(MG == 4 ? 512 : 256), lds, s, a, n_tiles, m_tiles);
