@@ -431,6 +431,7 @@ hipError_t launch_epi(const GemmArgs &a, hipStream_t s) {
   const int bn = tile_n(a.N, a.K, EPI);
   const int n_tiles = (a.N + bn - 1) / bn;
   if (a.b_tiled) return launch_gemm_stream(a, s);  // tiled weights: K % 64 == 0 by contract
+  if (a.a_gather && !(a.group_off && a.K % 64 == 0)) return hipErrorInvalidValue;  // only the streaming kernel gathers
   if (a.group_off) {
     // Expert row groups average B*k/E rows (64 at the MoE workload). The
     // streaming kernel takes them when K is a whole number of 64-wide steps

@@ -164,7 +164,9 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
 #pragma unroll
     for (int q = 0; q < AL; ++q) {
       const int m = min(m0 + wm * 64 + (wn * AL + q) * 8 + (lane >> 3), m_last - 1);
-      aptr[q] = p.A + (int64_t)m * p.lda + (int64_t)s_begin * BK + chunk;
+      int64_t row = m;
+      if (p.a_gather) row = min(max(p.a_gather[m] / p.a_gather_div, 0), p.a_gather_rows - 1);  // device data: clamp
+      aptr[q] = p.A + row * p.lda + (int64_t)s_begin * BK + chunk;
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i)

@@ -48,7 +48,7 @@ hipError_t execute(const Launch &L, hipStream_t s) {
     case LK_TOPK: return launch_topk(L.logits, L.rows, L.E, L.k, L.ids, L.weights, s);
     case LK_PERMUTE: {
       const hipError_t e = launch_permute(L.ids, L.rows, L.k, L.E, L.perm, L.slot_pos, L.expert_off, s);
-      if (e != hipSuccess) return e;
+      if (e != hipSuccess || !L.xp) return e;  // no xp: the expert GEMM that follows gathers its rows
       return launch_gather_rows(L.x, L.perm, L.expert_off + L.E, L.rows * L.k, L.k, L.width, L.xp, s);
     }
     case LK_COMBINE: return launch_moe_combine(L.x, L.weights, L.slot_pos, L.rows, L.k, L.width, L.out, s);

@@ -307,6 +307,15 @@ bool next_is(const ods_block *blk, int g, int op_end, OpKind k) {
   return a.layer == b.layer && b.kind == k;
 }
 
+// The expert gate_up GEMM reads its rows of hn through perm (no xp copy)
+// when moe_permute precedes it in the same range and the streaming kernel
+// runs it (K % 64 == 0).
+bool gather_fused(const ods_block *blk, int g_permute, int op_end) {
+  const OpRef op = op_at(blk, g_permute);
+  return op.kind == K_PERMUTE && next_is(blk, g_permute, op_end, K_EXP_GATE_UP) &&
+         blk->layers[op.layer].cfg.hidden % 64 == 0;
+}
+
 }  // namespace
 
 ods_status validate_range(const ods_block *blk, int op_begin, int op_end, const ods_batch *batch,
@@ -375,7 +384,12 @@ ods_status validate_range(const ods_block *blk, int op_begin, int op_end, const 
         add(st->expert_off, "expert_off"); add(st->xp, "xp");
         break;
       case K_EXP_GATE_UP:
-        add(st->xp, "xp");
+        if (g > op_begin && gather_fused(blk, g - 1, op_end)) {
+          add(st->hn, "hn");
+          add(st->perm, "perm");
+        } else {
+          add(st->xp, "xp");
+        }
         add(st->expert_off, "expert_off");
         add(L.w_gate_up, "w_gate_up");
         if (fuse_silu) add(st->act_p, "act_p"); else add(st->gu_p, "gu_p");
@@ -421,7 +435,6 @@ ods_status validate_range(const ods_block *blk, int op_begin, int op_end, const 
 
 void plan_launch(const ods_block *blk, int op_begin, int op_end, int i, const ods_batch *batch, const ods_state *st,
                  int cus, Launch *out) {
-  (void)op_begin;
   const int g = op_begin + i;
   const OpRef op = op_at(blk, g);
   const ods_layer &L = blk->layers[op.layer];
@@ -533,7 +546,8 @@ void plan_launch(const ods_block *blk, int op_begin, int op_end, int i, const od
     case K_PERMUTE:
       o.kind = LK_PERMUTE;
       o.ids = st->topk_ids; o.rows = B; o.k = c.top_k; o.E = c.n_experts; o.perm = st->perm;
-      o.slot_pos = st->slot_pos; o.expert_off = st->expert_off; o.x = U(st->hn); o.width = H; o.xp = U(st->xp);
+      o.slot_pos = st->slot_pos; o.expert_off = st->expert_off; o.x = U(st->hn); o.width = H;
+      o.xp = gather_fused(blk, g, op_end) ? nullptr : U(st->xp);  // null: the expert GEMM gathers
       break;
     case K_EXP_GATE_UP:
     case K_EXP_DOWN: {
@@ -548,11 +562,16 @@ void plan_launch(const ods_block *blk, int op_begin, int op_end, int i, const od
       ga.b_tiled = wt ? 1 : 0;
       if (op.kind == K_EXP_GATE_UP) {
         ga.A = U(st->xp); ga.lda = H; ga.K = H;
+        if (g > op_begin && gather_fused(blk, g - 1, op_end)) {
+          ga.A = U(st->hn);
+          ga.a_gather = st->perm; ga.a_gather_div = c.top_k; ga.a_gather_rows = B;
+          o.what = fuse ? "expert_gate_up+silu_mul (rows gathered by perm)" : "expert_gate_up (rows gathered by perm)";
+        }
         ga.B = U(L.w_gate_up); ga.ldb = H;
         ga.b_group_stride = wt ? tiled_weight_elems(I, H, true, 1) : (int64_t)2 * I * H;
         if (fuse) {
           ga.C = st->act_p; ga.ldc = I; ga.N = I; ga.n_up = I; ga.epi = EPI_SILU;
-          o.what = "expert_gate_up+silu_mul";
+          if (!ga.a_gather) o.what = "expert_gate_up+silu_mul";
           o.n_ops = 2;
         } else {
           ga.C = st->gu_p; ga.ldc = 2 * I; ga.N = 2 * I; ga.n_up = wt ? I : 0; ga.epi = EPI_BF16;

@@ -42,6 +42,9 @@ struct GemmArgs {
   int defer_reduce;           // splits > 1: leave the partials for a consumer that sums them itself
   int b_tiled;                // B in the streaming kernel's tile order (tile_weight); with n_up > 0
                               // the tiles pair gate and up rows, whatever the epilogue
+  const int32_t *a_gather;    // streaming kernel only: row r of A is row a_gather[r] / a_gather_div
+  int a_gather_div;           //   of the A pointer (clamped to [0, a_gather_rows)), e.g. the token
+  int a_gather_rows;          //   of an expert slot, read straight from hn
 };
 
 constexpr int kDecodeBM = 64, kDecodeBK = 128;  // decode-tile GEMM block rows and K step

@@ -186,7 +186,9 @@ def test_moe_skewed_groups(batch, tiled):
     expert 1 none (an empty group) and the rest share the remainder. At batch
     300 (75 rows per expert on average) the 128-row tile takes expert 0 in two
     passes; at batch 450 (112.5) the 256-row tile takes it in one. Every
-    token's residual against the oracle on the same ids and weights."""
+    token's residual against the oracle on the same ids and weights, and bit
+    for bit the same whether the expert GEMM gathers its rows of hn through
+    perm (one range) or reads the materialised xp (cut after moe_permute)."""
     w = replace(MOE_TILED, batch=batch)
     cfg = w.layers[0]
     E, k, H = cfg.n_experts, cfg.top_k, cfg.hidden
@@ -207,6 +209,17 @@ def test_moe_skewed_groups(batch, tiled):
     s.buf("topk_w", batch, k).copy_(torch.from_numpy(wts))
     s.run(9, 14)
     torch.cuda.synchronize()
+    fused = s.buf("resid", batch, H).clone()
+    # cut after moe_permute: xp is materialised and the expert GEMM reads it
+    # instead of gathering hn rows through perm; the result must not change
+    s.reset_resid()
+    s.run(9, 10)
+    s.run(10, 14)
+    torch.cuda.synchronize()
+    xp = s.buf("xp", batch * k, H)
+    perm = s.buf("perm", batch * k).long()
+    assert torch.equal(xp, hn[perm // k])
+    assert torch.equal(s.buf("resid", batch, H).view(torch.int16), fused.view(torch.int16))
     inp = s.oracle_inputs()
     live = {"resid": inp["x"].copy(), "hn": f64(hn), "topk_ids": ids.astype(np.int64),
             "topk_w": wts.astype(np.float64)}
