@@ -13,9 +13,13 @@ namespace ods {
 namespace {
 
 // One wave per token: top-k of the fp32 logits (ties -> lower expert id), and
-// softmax over the chosen k. E <= 256 (four logits per lane), k <= 64.
+// softmax over the chosen k. E <= 256 (four logits per lane), k <= 64. With
+// splits > 1 the token's logits are the sum of the router's split-K partials,
+// added in split order as the reduce would, and are written to logits_out.
 __global__ __launch_bounds__(256) void topk_kernel(const float *__restrict__ logits, int B, int E, int k,
-                                                   int32_t *__restrict__ ids, float *__restrict__ w) {
+                                                   int32_t *__restrict__ ids, float *__restrict__ w,
+                                                   const float *__restrict__ partial, int splits,
+                                                   float *__restrict__ logits_out) {
   const int lane = threadIdx.x & 63;
   const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (b >= B) return;
@@ -24,8 +28,17 @@ __global__ __launch_bounds__(256) void topk_kernel(const float *__restrict__ log
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int e = lane + 64 * j;
-    v[j] = e < E ? logits[(int64_t)b * E + e] : -INFINITY;
     taken[j] = e >= E;
+    if (e >= E) {
+      v[j] = -INFINITY;
+    } else if (splits > 1) {
+      float t = 0.f;
+      for (int sp = 0; sp < splits; ++sp) t += partial[((int64_t)sp * B + b) * E + e];
+      v[j] = t;
+      logits_out[(int64_t)b * E + e] = t;
+    } else {
+      v[j] = logits[(int64_t)b * E + e];
+    }
   }
   float z0 = 0.f, sum = 0.f, my_z = 0.f;
   int my_i = 0;
@@ -211,9 +224,12 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(const uint16_t *__rest
 
 }  // namespace
 
-hipError_t launch_topk(const float *logits, int B, int E, int k, int32_t *ids, float *w, hipStream_t s) {
+hipError_t launch_topk(const float *logits, int B, int E, int k, int32_t *ids, float *w, hipStream_t s,
+                       const float *partial, int splits, float *logits_out) {
   if (B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(topk_kernel, dim3((B + 3) / 4), dim3(256), 0, s, logits, B, E, k, ids, w);
+  if (splits > 1 && (!partial || !logits_out)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(topk_kernel, dim3((B + 3) / 4), dim3(256), 0, s, logits, B, E, k, ids, w, partial,
+                     splits > 1 ? splits : 1, logits_out);
   return hipGetLastError();
 }
 

@@ -45,7 +45,11 @@ hipError_t launch_attention(const uint16_t *qkv, int B, int n_q, int n_kv, int D
 
 hipError_t launch_silu_mul(const uint16_t *gu, uint16_t *act, int rows, int F, hipStream_t s);
 
-hipError_t launch_topk(const float *logits, int B, int E, int k, int32_t *ids, float *w, hipStream_t s);
+// Top-k routing of fp32 logits. With splits > 1 the logits are first summed
+// from the router's split-K partials [splits][B][E] (the split-K reduce's
+// order) and written to logits_out.
+hipError_t launch_topk(const float *logits, int B, int E, int k, int32_t *ids, float *w, hipStream_t s,
+                       const float *partial = nullptr, int splits = 1, float *logits_out = nullptr);
 hipError_t launch_permute(const int32_t *ids, int B, int k, int E, int32_t *perm, int32_t *slot_pos,
                           int32_t *expert_off, hipStream_t s);
 hipError_t launch_gather_rows(const uint16_t *src, const int32_t *perm, const int32_t *valid_rows,

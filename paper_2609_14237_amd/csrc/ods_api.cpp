@@ -46,6 +46,11 @@ hipError_t execute(const Launch &L, hipStream_t s) {
     }
     case LK_SILU: return launch_silu_mul(L.x, L.out, L.rows, L.width, s);
     case LK_TOPK: return launch_topk(L.logits, L.rows, L.E, L.k, L.ids, L.weights, s);
+    case LK_ROUTER_TOPK: {
+      const hipError_t e = launch_gemm(L.gemm, s);
+      if (e != hipSuccess) return e;
+      return launch_topk(nullptr, L.rows, L.E, L.k, L.ids, L.weights, s, L.topk_partial, L.topk_splits, L.logits_out);
+    }
     case LK_PERMUTE: {
       const hipError_t e = launch_permute(L.ids, L.rows, L.k, L.E, L.perm, L.slot_pos, L.expert_off, s);
       if (e != hipSuccess || !L.xp) return e;  // no xp: the expert GEMM that follows gathers its rows

@@ -542,7 +542,20 @@ void plan_launch(const ods_block *blk, int op_begin, int op_end, int i, const od
       o.width = op.kind == K_SILU ? c.ffn : c.moe_ffn;
       break;
     case K_DOWN: dense_gemm(st->act, L.w_down, st->resid, H, c.ffn, EPI_RESID, 0, H, false, wt); break;
-    case K_ROUTER: dense_gemm(st->hn, L.w_router, st->logits, c.n_experts, H, EPI_F32, 0, c.n_experts, false, false); break;
+    case K_ROUTER: {
+      // With split-K and top-k next in the range, the top-k kernel sums the
+      // partials itself (same order as the reduce) and writes the logits.
+      const bool fuse = next_is(blk, g, op_end, K_TOPK) && gemm_splits(B, c.n_experts, H, EPI_F32, false) > 1;
+      dense_gemm(st->hn, L.w_router, st->logits, c.n_experts, H, EPI_F32, 0, c.n_experts, fuse, false);
+      if (fuse) {
+        o.kind = LK_ROUTER_TOPK;
+        o.rows = B; o.E = c.n_experts; o.k = c.top_k; o.ids = st->topk_ids; o.weights = st->topk_w;
+        o.logits_out = st->logits; o.topk_partial = (const float *)st->ws; o.topk_splits = o.gemm.splits;
+        o.what = "router+topk_softmax";
+        o.n_ops = 2;
+      }
+      break;
+    }
     case K_TOPK:
       o.kind = LK_TOPK;
       o.logits = st->logits; o.rows = B; o.E = c.n_experts; o.k = c.top_k; o.ids = st->topk_ids; o.weights = st->topk_w;

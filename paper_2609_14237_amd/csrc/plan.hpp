@@ -115,7 +115,8 @@ ods_status validate_range(const ods_block *blk, int op_begin, int op_end, const 
 
 // One launch of a validated range.
 enum LaunchKind {
-  LK_RMSNORM, LK_GEMM, LK_QKV_ROPE, LK_ROPE_APPEND, LK_ATTENTION, LK_SILU, LK_TOPK, LK_PERMUTE, LK_COMBINE
+  LK_RMSNORM, LK_GEMM, LK_QKV_ROPE, LK_ROPE_APPEND, LK_ATTENTION, LK_SILU, LK_TOPK, LK_ROUTER_TOPK, LK_PERMUTE,
+  LK_COMBINE
 };
 struct RopeArgs {
   uint16_t *qkv; int B, n_q, n_kv, D; float theta;
@@ -135,13 +136,14 @@ struct Launch {
   int layer;
   int n_ops;         // operators this launch covers (more than one when fused)
   const char *what;  // static name for traces and errors
-  GemmArgs gemm;     // LK_GEMM, LK_QKV_ROPE
+  GemmArgs gemm;     // LK_GEMM, LK_QKV_ROPE, LK_ROUTER_TOPK
   RopeArgs rope;     // LK_QKV_ROPE, LK_ROPE_APPEND
   AttnArgs attn;     // LK_ATTENTION
   // LK_RMSNORM: x -> out with gain; LK_SILU: x (gate | up) -> out; LK_COMBINE: x (yp) into out (resid)
   const uint16_t *x, *gain; uint16_t *out; int rows, width; float eps;
-  // LK_TOPK, LK_PERMUTE, LK_COMBINE
+  // LK_TOPK, LK_ROUTER_TOPK, LK_PERMUTE, LK_COMBINE
   const float *logits; float *weights; int32_t *ids, *perm, *slot_pos, *expert_off; int E, k;
+  float *logits_out; const float *topk_partial; int topk_splits;  // LK_ROUTER_TOPK: router split-K partials
   uint16_t *xp;
 };
 

@@ -305,6 +305,7 @@ def test_moe_layer_small_and_cuts():
     rng = np.random.default_rng(7)
     cut_sets = [[], [6], [3, 5], [7], [8], [9], [10], [11], [12], [13]] + \
                [sorted(rng.choice(np.arange(1, 14), 3, replace=False).tolist()) for _ in range(4)]
+    first_logits = None
     for cut in cut_sets:
         say("moe cut", cut)
         s.reset_resid()
@@ -312,9 +313,15 @@ def test_moe_layer_small_and_cuts():
         for a, b in zip(bounds[:-1], bounds[1:]):
             s.run(a, b)
         torch.cuda.synchronize()
+        # the router's split-K sum is the same whether the reduce kernel or the
+        # top-k kernel (router and top-k in one range) does it: bit for bit
+        raw = s.buf("logits", w.batch, 64).clone()
+        if first_logits is None:
+            first_logits = raw
+        assert torch.equal(raw.view(torch.int32), first_logits.view(torch.int32)), f"logits differ at cut {cut}"
         ids = s.buf("topk_ids", w.batch, cfg.top_k).cpu().numpy()
         wts = f64(s.buf("topk_w", w.batch, cfg.top_k))
-        logits = f64(s.buf("logits", w.batch, 64))
+        logits = f64(raw)
         forced, summary = routing_check(f"moe cut {cut}", ids, wts, logits, ref, cfg.top_k)
         assert_close(f"logits {cut}", logits, ref["logits"])
         # the residual of every token, with the oracle evaluated on the GPU's
