@@ -242,7 +242,10 @@ const char *ods_op_name(const ods_block *blk, int32_t op);
 /* Enqueue operators [op_begin, op_end) of the block on `stream` (one native
  * submission for one stage; Section 6). Adjacent operators inside the range
  * may be fused; every buffer of the live set at op_end is materialised, so a
- * block run as any sequence of contiguous ranges computes the same step.
+ * block run as any sequence of contiguous ranges computes the same step. A
+ * buffer consumed inside the range may be left unwritten (with moe_permute
+ * and expert_gate_up in one range the expert GEMM reads hn through perm and
+ * xp is not written).
  * ODS_ERANGE unless 0 <= op_begin < op_end <= ods_block_num_ops(). An empty
  * batch (batch->batch == 0) returns ODS_OK once the block and the range are
  * valid, enqueueing nothing and reading no pointer of batch or state. */
