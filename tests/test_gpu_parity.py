@@ -334,6 +334,43 @@ def test_moe_layer_small_and_cuts():
     report(f"moe_small (batch {w.batch}) cuts: routing {summary}")
 
 
+MOE_K8 = W.Workload("moe_k8", (W.LayerCfg(hidden=520, n_q=8, n_kv=2, head_dim=64, n_experts=16, top_k=4,
+                                           moe_ffn=136),), batch=40, ctx_lo=1, ctx_hi=200, router_std=520 ** -0.5)
+
+
+def test_moe_layer_hidden_not_multiple_of_64():
+    """hidden 520 and expert width 136 (multiples of 8, not of 64): the expert
+    GEMMs take the register-staged large-M tile, so moe_permute gathers xp
+    even when expert_gate_up shares its range; the whole layer and the cut
+    after moe_permute against the oracle, and bit for bit against each other."""
+    w = MOE_K8
+    cfg = w.layers[0]
+    s = Setup(w, seed=9)
+    inp = s.oracle_inputs()
+    ref = oracle_run(fresh(inp), w.layers, 0, 14)
+    pre = oracle_run(fresh(inp), w.layers, 0, 9)
+    outs = []
+    for cut in ([], [10]):
+        say("moe hidden 520 cut", cut)
+        s.reset_resid()
+        bounds = [0] + cut + [14]
+        for a, b in zip(bounds[:-1], bounds[1:]):
+            s.run(a, b)
+        torch.cuda.synchronize()
+        ids = s.buf("topk_ids", w.batch, cfg.top_k).cpu().numpy()
+        wts = f64(s.buf("topk_w", w.batch, cfg.top_k))
+        logits = f64(s.buf("logits", w.batch, cfg.n_experts))
+        forced, summary = routing_check(f"moe hidden 520 cut {cut}", ids, wts, logits, ref, cfg.top_k)
+        live = {"resid": pre["resid"].copy(), "hn": pre["hn"], "topk_ids": forced,
+                "topk_w": O.route_weights(ref["logits"], forced)}
+        ref2 = oracle_run(fresh(inp), w.layers, 9, 14, live)
+        out = s.buf("resid", w.batch, cfg.hidden).clone()
+        assert_close(f"resid {cut}", f64(out), ref2["resid"])
+        outs.append(out)
+    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+    report(f"moe_k8 (hidden 520, batch {w.batch}): routing {summary}")
+
+
 # ---------------------------------------------------------------- hybrid block and real shapes
 
 HYBRID_SMALL = W.Workload("hybrid_small",
