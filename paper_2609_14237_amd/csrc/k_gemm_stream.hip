@@ -48,8 +48,9 @@ constexpr int kStageRow = 132;
 // step t "vmcnt <= loads of NSLOT - 2 steps" means this wave's loads of step
 // t + 1 have landed, and the barrier that follows publishes every wave's
 // share. The loads of step t + NSLOT are issued after that barrier, into the
-// slot of step t, whose fragments are in registers by then. The barrier is a bare s_barrier (the workgroup fence of
-// __syncthreads would wait for every load in flight).
+// slot of step t, whose fragments are in registers by then. The barrier is a
+// bare s_barrier (the workgroup fence of __syncthreads would wait for every
+// load in flight).
 //
 // Blocks are placed so that the compute units of one XCD share a K range
 // (split-K) and the M tiles of one weight slab run on one XCD at the same
@@ -111,10 +112,10 @@ void gemm_stream_kernel(GemmArgs p, int n_tiles, int m_tiles) {
   const bool b_once = (MG == 1 || p.splits == 1) && (p.group_off ? m_last - m_first <= BM : m_tiles == 1);
   // The staged epilogue stores whole 16-byte chunks: every chunk must lie
   // inside or outside the output columns, and start 16-byte aligned.
-  constexpr int CW_ = PARTIAL || EPI == EPI_F32 ? 4 : 8;
+  constexpr int VEC_W = PARTIAL || EPI == EPI_F32 ? 4 : 8;  // outputs per chunk
   const int n_lim = !SILU && p.b_tiled && p.n_up > 0 ? p.n_up : p.N;
-  const bool vec = p.N % CW_ == 0 && n_lim % CW_ == 0 &&
-                   (PARTIAL ? ((uintptr_t)p.partial & 15) == 0 : p.ldc % CW_ == 0 && ((uintptr_t)p.C & 15) == 0);
+  const bool vec = p.N % VEC_W == 0 && n_lim % VEC_W == 0 &&
+                   (PARTIAL ? ((uintptr_t)p.partial & 15) == 0 : p.ldc % VEC_W == 0 && ((uintptr_t)p.C & 15) == 0);
 
   const int steps = p.K / BK;
   const int per = (steps + p.splits - 1) / p.splits;
