@@ -254,7 +254,7 @@ ods_status ods_run_partition(const ods_block *blk, int32_t op_begin, int32_t op_
 
 /* Size of the workspace the library itself holds on each device for
  * ods_run_partition_scratch (64 MiB; every evaluated block needs at most
- * 40 MiB, as ods_workspace_bytes reports). */
+ * 32 MiB, as ods_workspace_bytes reports). */
 #define ODS_SCRATCH_BYTES ((size_t)64 << 20)
 
 /* For callers that cannot allocate device memory (code under HIP graph
