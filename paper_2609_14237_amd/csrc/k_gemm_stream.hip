@@ -432,7 +432,9 @@ hipError_t launch_stream(const GemmArgs &a, hipStream_t s) {
 
 // Tile shapes. Dense GEMMs: 64-row tiles (two blocks per CU) up to 64 rows,
 // 256-row tiles past that (at 96 and 128 rows the 256-row tile with idle
-// waves beats the 128-row one on every 8B-shaped GEMM, by 3-14 us). Grouped
+// waves beats the 128-row one on every 8B-shaped GEMM, by 3-14 us), except
+// where the 256-row grid would leave most compute units idle
+// (gemm_stream_rows: 64-row tiles again). Grouped
 // (expert) GEMMs, by the average rows per group:
 //  - up to 32: 64-row tiles;
 //  - up to 96: 128-row tiles (two blocks per CU on a two-slot ring), which
@@ -449,7 +451,7 @@ StreamTile gemm_stream_tile(const GemmArgs &a) {
     if (a.groups <= 0 || a.M <= 32 * a.groups) return TILE_64;
     return a.M <= 96 * a.groups ? TILE_128 : TILE_256;
   }
-  return a.M <= 64 ? TILE_64 : TILE_256;
+  return gemm_stream_rows(a.M, a.N, a.K, a.epi) == 64 ? TILE_64 : TILE_256;
 }
 
 template <int MG, int NSLOT, int EPI>

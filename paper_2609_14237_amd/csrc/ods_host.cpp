@@ -143,20 +143,48 @@ bool gemm_use_stream(int M, int N, int K, int epi) {
   return M > 128 || (M > 32 && M <= 64 && epi != EPI_SILU);
 }
 
+namespace {
+
 // Split K (1, 2, 4 or 8 ways, at least 8 steps per split) while the blocks
 // still fit one wave over the 256 compute units (the 256-row tile runs one
 // block per CU, so 257 to 511 blocks would leave a mostly idle second wave:
 // the MoE layer's qkv projection at 512 rows, 80 tiles, took 53 us with 4
-// splits against 40 us with 2, reduce included); the reduce works on
-// 4-column groups.
-int gemm_stream_splits(int M, int N, int K, int epi) {
-  if (N % 4 != 0) return 1;
-  const int bn = epi == EPI_SILU ? 64 : 128;
-  const int tiles = ((M + 255) / 256) * ((N + bn - 1) / bn);
-  const int steps = K / 64;
+// splits against 40 us with 2, reduce included).
+int stream_splits(int tiles, int steps) {
   int s = 1;
   while (tiles * s * 2 <= 256 && s < 8 && steps / (s * 2) >= 8) s *= 2;
   return s;
+}
+
+int stream_n_tiles(int N, int epi) { return epi == EPI_SILU ? (N + 63) / 64 : (N + 127) / 128; }
+
+}  // namespace
+
+// Past 64 rows a dense GEMM takes the 256-row tile unless that grid, split-K
+// included, would occupy fewer than half of the 256 compute units (small
+// weights: a tensor-parallel share of a layer, a narrow model). Then 64-row
+// tiles give it ceil(M / 64) times the blocks, and the blocks of one N tile
+// read its weights through one XCD's L2. Measured at M = 256 on one GPU's
+// share of the 8B-shaped layer under 8-way tensor parallelism (lab, tiled
+// weights, reduce included; 256-row -> 64-row tile): qkv (N 768, 48 -> 192
+// blocks) 13.0 -> 8.3 us, o_proj (K 512, 32 -> 128 blocks) 12.9 -> 7.9 us,
+// down (K 1792, 64 -> 256 blocks) 23.7 -> 17.2 us; gate_up + SiLU (N 1792)
+// keeps 224 256-row blocks (24.3 us; 22.9 us as 64-row tiles). With 192 or
+// more 256-row blocks the 256-row tile stays ahead (the 8B-shaped layer's
+// GEMMs at M = 256: gate_up 81 against 113 us, down 48-51 against 62-64 us
+// as 64-row tiles).
+int gemm_stream_rows(int M, int N, int K, int epi) {
+  if (M <= 64) return 64;
+  const int tiles = (M + 255) / 256 * stream_n_tiles(N, epi);
+  const int s = N % 4 != 0 ? 1 : stream_splits(tiles, K / 64);
+  return tiles * s < 128 ? 64 : 256;
+}
+
+// The reduce works on 4-column groups: other widths run unsplit.
+int gemm_stream_splits(int M, int N, int K, int epi) {
+  if (N % 4 != 0) return 1;
+  const int rows = gemm_stream_rows(M, N, K, epi);
+  return stream_splits((M + rows - 1) / rows * stream_n_tiles(N, epi), K / 64);
 }
 
 int gemm_splits(int M, int N, int K, int epi, bool b_tiled) {

@@ -56,6 +56,7 @@ int tile_n(int N, int K, int epi);     // decode tile width
 // Weight-streaming kernel: dense GEMMs past 128 rows, of 33 to 64 rows but
 // the SiLU-gated one, grouped GEMMs, and every GEMM on tiled weights.
 bool gemm_use_stream(int M, int N, int K, int epi);
+int gemm_stream_rows(int M, int N, int K, int epi);  // dense block rows: 64 or 256
 int gemm_stream_splits(int M, int N, int K, int epi);
 // Split-K plan of a dense GEMM, and the fp32 partial bytes it needs.
 int gemm_splits(int M, int N, int K, int epi, bool b_tiled = false);

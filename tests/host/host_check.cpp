@@ -221,6 +221,29 @@ static std::vector<Work> read_works(const char *path) {
   return out;
 }
 
+// Block rows and split-K of the dense streaming GEMM at the shapes the
+// tile rule was measured on: the 8B-shaped layer at 256 rows keeps the
+// 256-row tile, one GPU's 8-way tensor-parallel share of it takes 64-row
+// tiles, and up to 64 rows every GEMM takes 64-row tiles.
+static void check_stream_tiles() {
+  struct Case {
+    int M, N, K, epi, rows, splits;
+  };
+  const Case cases[] = {
+      {256, 14336, 4096, EPI_SILU, 256, 1}, {256, 4096, 14336, EPI_RESID, 256, 8},
+      {256, 6144, 4096, EPI_BF16, 256, 4},  {256, 4096, 4096, EPI_RESID, 256, 8},
+      {256, 1792, 4096, EPI_SILU, 256, 8},   {256, 4096, 1792, EPI_RESID, 64, 2},
+      {256, 768, 4096, EPI_BF16, 64, 8},    {256, 4096, 512, EPI_RESID, 64, 1},
+      {64, 14336, 4096, EPI_SILU, 64, 1},   {64, 4096, 4096, EPI_RESID, 64, 8},
+      {512, 4096, 4096, EPI_RESID, 256, 4}, {512, 5120, 4096, EPI_BF16, 256, 2},
+      {200, 9000, 512, EPI_SILU, 256, 1},   {200, 896, 640, EPI_BF16, 64, 1},
+  };
+  for (const Case &c : cases) {
+    CHECK(gemm_stream_rows(c.M, c.N, c.K, c.epi) == c.rows);
+    CHECK(gemm_stream_splits(c.M, c.N, c.K, c.epi) == c.splits);
+  }
+}
+
 int main(int argc, char **argv) {
   if (argc < 2) {
     fprintf(stderr, "usage: host_check workloads.txt\n");
@@ -228,6 +251,7 @@ int main(int argc, char **argv) {
   }
   check_allocator();
   check_bad_configs();
+  check_stream_tiles();
   for (Work &w : read_works(argv[1])) {
     for (int tiled = 0; tiled < 2; ++tiled) {
       for (ods_layer &L : w.layers) L.weight_layout = tiled ? ODS_WEIGHTS_TILED : ODS_WEIGHTS_ROWS;

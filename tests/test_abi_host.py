@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(B.SIGNATURES)
 
 
-@pytest.mark.parametrize("w", W.ALL, ids=lambda w: w.name)
+@pytest.mark.parametrize("w", W.ALL + W.SHARES, ids=lambda w: w.name)
 def test_kv_alloc_matches_oracle_bit_exactly(w):
     ctx = gen.contexts(w)
     P = gen.pool_pages_for(ctx)
@@ -284,7 +284,7 @@ def test_scratch_entry_point_validates_before_touching_the_device():
     assert B.ods_run_partition_scratch(big.c, 0, 10, batch, fake_state(ws=None, ws_bytes=0), 0) == B.ODS_ENOMEM
     assert "scratch" in B.ods_last_error()
     # every evaluated block fits
-    for w in W.ALL:
+    for w in W.ALL + W.SHARES:
         blk = fake_block(w.layers)
         assert 0 < B.ods_workspace_bytes(blk.c, fake_batch(w.batch, w.max_pages)) <= B.SCRATCH_BYTES, w.name
 

@@ -63,6 +63,7 @@ CHAINED_BAR = {
     "dense8b_b256_ctx8k": {"resid": 1e-2, "o": O_BAR},
     "hybrid4_b128": {"resid": 2e-2, "o": 4e-2},
     "moe64x8_b512": {"resid": 1e-2, "o": O_BAR},
+    "dense8b_b256_ctx8k_tp8": {"resid": 1e-2, "o": O_BAR},
 }
 
 
@@ -291,7 +292,8 @@ def chained(f):
 
 
 @pytest.mark.parametrize("tiled", [True, False], ids=["tiled", "rows"])
-@pytest.mark.parametrize("name", ["dense8b_b64", "dense8b_b256_ctx8k", "hybrid4_b128", "moe64x8_b512"])
+@pytest.mark.parametrize("name", ["dense8b_b64", "dense8b_b256_ctx8k", "hybrid4_b128", "moe64x8_b512",
+                                  "dense8b_b256_ctx8k_tp8"])
 def test_fullsize(name, tiled):
     w = W.BY_NAME[name]
     f = FullSize(w, tiled)

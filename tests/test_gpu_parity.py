@@ -416,9 +416,11 @@ def test_dense_8b_shape_small_batch():
 
 @pytest.mark.parametrize("batch", [65, 100, 128, 200, 300])
 def test_layer_across_gemm_tile_paths(batch):
-    """Batches above 64 rows take the 512-thread large-M GEMM tiles (128 rows up
-    to 128, 256 rows above); F = 688 leaves K and SiLU-N tails, H = 640 an
-    N tail of the 128-column tile."""
+    """Batches above 64 rows take the 512-thread large-M GEMM tiles up to 128
+    rows; past 128 the streaming kernel runs every GEMM whose K is a multiple
+    of 64, on 64-row tiles at these narrow widths, and down (K = 688) stays on
+    the 256-row large-M tile. F = 688 leaves K and SiLU-N tails, H = 640 an N
+    tail of the 128-column tile."""
     cfg = W.LayerCfg(hidden=640, n_q=10, n_kv=2, head_dim=64, ffn=688)
     w = W.Workload("gemm_paths", (cfg,), batch=batch, ctx_lo=1, ctx_hi=70)
     say("gemm tile paths, batch", batch)
@@ -438,6 +440,32 @@ def test_layer_across_gemm_tile_paths(batch):
     torch.cuda.synchronize()
     assert_close("gu", f64(s.buf("gu", batch, 2 * cfg.ffn)), ref["gu"])
     assert_close("resid (split at silu)", f64(s.buf("resid", batch, cfg.hidden)), ref["resid"])
+
+
+@pytest.mark.parametrize("ffn,tiled", [(9000, False), (8960, True)], ids=["rows", "tiled"])
+def test_wide_gated_ffn_on_256_row_stream_tiles(ffn, tiled):
+    """An FFN wide enough to fill the compute units with 256-row streaming
+    tiles at 200 rows: 141 gated tiles of 64 columns (row-major F = 9000
+    leaves a 40-column tail; tiled F = 8960 gives 140) for gate_up + SiLU,
+    and as many 128-column tiles (an 80-column tail row-major) for the
+    unfused gate_up's bf16 epilogue."""
+    cfg = W.LayerCfg(hidden=512, n_q=8, n_kv=2, head_dim=64, ffn=ffn)
+    w = W.Workload("wide_ffn", (cfg,), batch=200, ctx_lo=1, ctx_hi=60)
+    say("wide gated FFN on 256-row stream tiles, batch 200, ffn", ffn, "tiled" if tiled else "rows")
+    s = Setup(w, seed=14, tiled=tiled)
+    ref = oracle_run(fresh(s.oracle_inputs()), w.layers, 0, 10)
+    s.reset_resid()
+    s.run(0, 10)
+    torch.cuda.synchronize()
+    _check_layer_buffers(s, ref, cfg, 200)
+    act = O.silu(ref["gu"][:, :cfg.ffn]) * ref["gu"][:, cfg.ffn:]
+    assert_close("act", f64(s.buf("act", 200, cfg.ffn)), act)
+    s.reset_resid()
+    s.run(0, 8)
+    s.run(8, 10)
+    torch.cuda.synchronize()
+    assert_close("gu", f64(s.buf("gu", 200, 2 * cfg.ffn)), ref["gu"])
+    assert_close("resid (split at silu)", f64(s.buf("resid", 200, cfg.hidden)), ref["resid"])
 
 
 @pytest.mark.parametrize("batch", [33, 47, 64])

@@ -4,8 +4,11 @@
   numpy rearrangement written from the layout's definition in include/ods.h.
 - A layer run on tiled weights matches the oracle (which takes the row-major
   weights) to the same 1e-2 bar as the row-major path, at batches that take
-  the 64-row and the 256-row streaming tiles, with N tails, split-K partials
-  and the unfused gate_up (whose plain epilogue un-pairs the gate and up rows).
+  64-row streaming tiles (one and several per N tile: at these narrow widths
+  a 256-row grid would leave most compute units idle), with N tails, split-K
+  partials and the unfused gate_up (whose plain epilogue un-pairs the gate
+  and up rows). The 256-row tile on tiled weights is covered by the wide-FFN
+  parity test and at full size.
 - Where the row-major path runs the same streaming kernel with the same
   split, both layouts give bit-identical results."""
 import sys

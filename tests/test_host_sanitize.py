@@ -19,7 +19,7 @@ CXX = os.environ.get("CXX", "g++")
 def test_host_part_is_clean_under_asan_and_ubsan(tmp_path):
     works = tmp_path / "workloads.txt"
     with open(works, "w") as fh:
-        for w in W.ALL:
+        for w in W.ALL + W.SHARES:
             fh.write(f"{w.name} {w.batch} {w.max_pages} {len(w.layers)}")
             for c in w.layers:
                 fh.write(f" {c.hidden} {c.n_q} {c.n_kv} {c.head_dim} {c.ffn} {c.n_experts} {c.top_k} "

@@ -111,7 +111,23 @@ MOE_B512 = Workload(
 )
 
 ALL = (TINY, DENSE_8B_B64, DENSE_8B_B256, HYBRID_4L, MOE_B512)
-BY_NAME = {w.name: w for w in ALL}
+
+# One GPU's share of the batch-256 x 8192 dense layer when the layer is split
+# 8 ways by tensor parallelism: attention by KV head (one KV head with its four
+# query heads, the matching slices of W_qkv and W_o), the SwiGLU FFN by
+# intermediate columns (1792 of 14336), the residual stream replicated. Its
+# outputs are the partial sums an all-reduce would complete; on one GPU the
+# same kernels run at exactly this shape.
+DENSE_8B_B256_TP8 = Workload(
+    name="dense8b_b256_ctx8k_tp8",
+    layers=(LayerCfg(hidden=4096, n_q=4, n_kv=1, head_dim=128, ffn=1792),),
+    batch=256, ctx_lo=8192, ctx_hi=8192,
+    description="one GPU's share of the batch-256 x 8192 8B-shaped layer under 8-way tensor "
+                "parallelism: hidden 4096, 4q/1kv x 128, SwiGLU 1792",
+)
+
+SHARES = (DENSE_8B_B256_TP8,)
+BY_NAME = {w.name: w for w in ALL + SHARES}
 
 
 def shrink(w: Workload, **kw) -> Workload:
