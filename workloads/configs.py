@@ -116,7 +116,8 @@ ALL = (TINY, DENSE_8B_B64, DENSE_8B_B256, HYBRID_4L, MOE_B512)
 # 8 ways by tensor parallelism: attention by KV head (one KV head with its four
 # query heads, the matching slices of W_qkv and W_o), the SwiGLU FFN by
 # intermediate columns (1792 of 14336), the residual stream replicated. Its
-# outputs are the partial sums an all-reduce would complete; on one GPU the
+# o_proj and down products are the partial sums an all-reduce would complete;
+# here they go straight into the residual (the same work per GPU), and the
 # same kernels run at exactly this shape.
 DENSE_8B_B256_TP8 = Workload(
     name="dense8b_b256_ctx8k_tp8",
