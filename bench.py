@@ -343,21 +343,30 @@ def ffn_sweep(args):
 def latency_table(args):
     """Profiled stage latencies t_j = f_lat(op range, batch, context), the
     per-stage inputs of the paper's communication-aware latency model (Section
-    4), for the dense 8B-shaped layer: every stage template at every (batch,
-    context) point, timed as a replay of its captured HIP graph and as an
-    eager ods_run_partition call (median of --steps each). One weight/KV copy:
-    small KV footprints partly stay in the 256 MB last-level cache."""
+    4), for the layer of a one-layer workload (--workload: the dense 8B-shaped
+    layer by default, or the MoE layer): every single operator and every stage
+    template at every (batch, context) point, the templates timed as a replay
+    of their captured HIP graph and as an eager ods_run_partition call (median
+    of --steps each). One weight/KV copy: small KV footprints partly stay in
+    the 256 MB last-level cache."""
     import torch
     import workloads as W
     from workloads import gen
     from paper_2609_14237_amd import binding as B
     from paper_2609_14237_amd import runtime as R
 
-    base = W.BY_NAME["dense8b_b64"]
+    base = W.BY_NAME[args.workload]
+    if len(base.layers) != 1:
+        sys.exit("--latency-table profiles one layer shape: choose a one-layer workload")
     cfg = base.layers[0]
+    n_ops = cfg.n_ops
     dev = "cuda"
     torch.cuda.set_device(0)
-    templates = [("attention stage", 0, 6), ("FFN stage", 6, 10), ("core attention", 3, 5), ("colocated layer", 0, 10)]
+    templates = [("attention stage", 0, 6), ("FFN stage", 6, n_ops), ("core attention", 3, 5),
+                 ("colocated layer", 0, n_ops)]
+    # the MoE layer's expert GEMMs stay bound by their weight stream far past
+    # 256 rows (its b* is about 2000), so its table goes further
+    batches = (1, 8, 32, 64, 128, 256) + ((512, 1024) if cfg.n_experts else ())
     weights = [gen.layer_weights(cfg, base.seed, 0, dev, base.router_std)]
     tiled = args.weights == "tiled"
     if tiled:
@@ -379,7 +388,7 @@ def latency_table(args):
 
     rows, op_rows = [], []
     for ctx_len in (1024, 4096, 16384):
-        for M in (1, 8, 32, 64, 128, 256):
+        for M in batches:
             ctx = np.full(M, ctx_len, dtype=np.int32)
             P = gen.pool_pages_for(ctx)
             max_pages = -(-ctx_len // 16)
@@ -390,7 +399,7 @@ def latency_table(args):
             blk = R.DeviceBlock([cfg], weights, pools, P, pretiled=tiled)
             st = R.DeviceState(blk, batch, dev)
             x = gen.activations(M, cfg.hidden, base.seed, dev)
-            for i in range(10):  # single operators, eager, for per-operator latency models
+            for i in range(n_ops):  # single operators, eager, for per-operator latency models
                 st.view("resid", M, cfg.hidden).copy_(x)
                 if i > 0:
                     R.run_partition(blk, 0, i, batch, st, stream)
@@ -410,8 +419,8 @@ def latency_table(args):
                       f"eager {t_eager:.1f} us", file=sys.stderr, flush=True)
             del blk, st, pools, batch
             torch.cuda.empty_cache()
-    print(json.dumps({"metric": "stage latency t_j = f_lat(op range, batch, context), dense 8B-shaped layer",
-                      "unit": "us", "steps": args.steps, "warmup": args.warmup, "dtype": "bf16",
+    print(json.dumps({"metric": "stage latency t_j = f_lat(op range, batch, context)", "workload": base.name,
+                      "layer": base.description, "unit": "us", "steps": args.steps, "warmup": args.warmup, "dtype": "bf16",
                       "data": "synthetic", "weight_layout": args.weights, "latency_table": rows,
                       "op_latency": op_rows}), flush=True)
 

@@ -18,20 +18,26 @@ x* = 2 P_act (gamma_1 - gamma_2) / (alpha_2 - alpha_1) of x = m_kv(s).
 
 Planner (Sections 4-5, Appendix B). A partition block of N ordered operators
 is cut by a contiguous template q = (0 = q_0 < ... < q_S = N); stage j runs on
-owner sigma(j) = ((j - 1) mod K) + 1 (here K = S, one stage position per
-owner). Stage latency t_j sums its operators' latencies at the per-replica
-microbatch b_hat (roofline estimates max(D / beta, W / F), or measured
-per-operator profiles); the transfer after stage j moves the live set at that
-cut, u_j = b_hat * A_j / link bandwidth. The round-trip time of mu
+owner type sigma(j) = ((j - 1) mod K) + 1 (here K = S, one stage position per
+type). Each type m has its own per-replica microbatch b_hat_m, so a global
+microbatch of B_hat requests takes n_m = B_hat / b_hat_m replicas of type m:
+a type with a larger microbatch gathers the microbatches of several replicas
+of the types before it (Appendix B, replica counts). Stage latency t_j sums
+its operators' latencies at the microbatch of its type (roofline estimates
+max(D / beta, W / F), or measured per-operator profiles); the transfer after
+stage j moves the live set at that cut, u_j = b_hat * A_j / link bandwidth
+with b_hat the larger of the two sides' microbatches (the side that gathers
+or scatters serializes them over its link). The round-trip time of mu
 microbatches over B_total blocks is taken as the larger of the two lower
 bounds the paper's branch-and-bound uses: the dependency chain of one
 microbatch, B_total * sum_j (t_j + u_j) (the last block's wrap-around transfer
 omitted), and the serialized work of the busiest resource, mu * B_total *
-t_j per owner and per link. A plan costs CPT = T_rtt * sum_m c_m / b_m with
-b_m = mu * b_hat, subject to T_rtt <= SLO and, per owner, weights of its
+t_j per replica and per link. A plan costs CPT = T_rtt * sum_m c_m / b_m with
+b_m = mu * b_hat_m, subject to T_rtt <= SLO and, per type, weights of its
 stages plus the KV of mu resident microbatches within M. The search is
 exhaustive over S, templates (and the block's rotation, so a stage may wrap
-the block boundary as CAD's rest-of-model stage does), mu and b_hat.
+the block boundary as CAD's rest-of-model stage does), mu and the
+microbatches: one shared by every type, or (per_type_batch) one per type.
 """
 from __future__ import annotations
 
@@ -347,12 +353,13 @@ class Plan:
     rotation: int
     q: tuple
     mu: int
-    b_hat: int
+    b_hat: int            # the largest per-replica microbatch of the plan's types
     t: list
     u: list
     t_rtt: float
     cpt: float
     memory: list = field(default_factory=list)
+    b_hats: tuple = ()    # per-replica microbatch of each stage's type
 
     @property
     def S(self) -> int:
@@ -376,15 +383,17 @@ class _Tables:
             self.by_b[b] = (pre(lat), pre(w), pre(kv), hand)
 
 
-def _plan_from_tables(model: Model, g: Gpu, tab: _Tables, q: tuple, mu: int, b_hat: int, rotation: int):
-    plat, pw, pkv, hand = tab.by_b[b_hat]
+def _plan_from_tables(model: Model, g: Gpu, tab: _Tables, q: tuple, mu: int, b_hat, rotation: int):
+    """b_hat: one per-replica microbatch for every type, or a tuple with one per stage."""
     S = len(q) - 1
+    bs = tuple(b_hat) if isinstance(b_hat, tuple) else (b_hat,) * S
     t, u, mem = [], [], []
     for j in range(S):
+        plat, pw, pkv, _ = tab.by_b[bs[j]]
         lo, hi = rotation + q[j], rotation + q[j + 1]
         t.append(plat[hi] - plat[lo])
-        u.append(hand[hi - 1] if S > 1 else 0.0)
-        need = (pw[hi] - pw[lo]) * model.n_blocks + mu * b_hat * (pkv[hi] - pkv[lo]) * model.n_blocks
+        u.append(tab.by_b[max(bs[j], bs[(j + 1) % S])][3][hi - 1] if S > 1 else 0.0)
+        need = (pw[hi] - pw[lo]) * model.n_blocks + mu * bs[j] * (pkv[hi] - pkv[lo]) * model.n_blocks
         if need > g.memory:
             return None
         mem.append(need)
@@ -394,8 +403,8 @@ def _plan_from_tables(model: Model, g: Gpu, tab: _Tables, q: tuple, mu: int, b_h
     if S > 1:
         loads.append(mu * (Bt - 1) * u[-1])
     t_rtt = max([chain] + loads)
-    cpt = t_rtt * S * g.c / (mu * b_hat)
-    return Plan(rotation, q, mu, b_hat, t, u, t_rtt, cpt, mem)
+    cpt = t_rtt * sum(g.c / (mu * b) for b in bs)
+    return Plan(rotation, q, mu, max(bs), t, u, t_rtt, cpt, mem, bs)
 
 
 def evaluate(model: Model, g: Gpu, q: tuple, mu: int, b_hat: int, s: float, latency: Callable | None = None,
@@ -409,17 +418,23 @@ def evaluate(model: Model, g: Gpu, q: tuple, mu: int, b_hat: int, s: float, late
 
 def search(model: Model, g: Gpu, s: float, slo: float, latency: Callable | None = None, S_max: int = 3,
            mus=(1, 2, 4, 8), b_hats=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), link_bw: float = 153e9,
-           rotations: bool = True):
-    """Every plan over the grid that meets the SLO and fits memory, cheapest first."""
+           rotations: bool = True, per_type_batch: bool = False, per_type_S_max: int = 2):
+    """Every plan over the grid that meets the SLO and fits memory, cheapest
+    first. With per_type_batch, plans of 2 to per_type_S_max stages also try
+    every combination of per-replica microbatches over their types."""
     tab = _Tables(model, g, s, latency or roofline_latency(g), b_hats, link_bw)
     N = tab.N
     out = []
     for S in range(1, S_max + 1):
         rots = range(N) if (rotations and S > 1) else (0,)
+        if per_type_batch and 1 < S <= per_type_S_max:
+            combos = list(itertools.product(b_hats, repeat=S))
+        else:
+            combos = list(b_hats)
         for r in rots:
             for q in templates(N, S):
                 for mu in mus:
-                    for b in b_hats:
+                    for b in combos:
                         p = _plan_from_tables(model, g, tab, q, mu, b, r)
                         if p is not None and p.t_rtt <= slo:
                             out.append(p)
@@ -439,34 +454,38 @@ def named_plans(model: Model):
 
 
 def profile_report(profile: dict, model: Model, g: Gpu, s: float, slo: float, S_max: int = 3,
-                   mus=(1, 2, 4, 8), b_hats=(1, 8, 32, 64, 128, 256)) -> str:
+                   mus=(1, 2, 4, 8), b_hats=(1, 8, 32, 64, 128, 256), per_type_batch: bool = False) -> str:
     """Markdown table: the cheapest plan of the exhaustive search and the best
     point of each named template, with per-operator latencies measured on the
-    GPU (profile["op_latency"])."""
+    GPU (profile["op_latency"]). With per_type_batch, plans of two stages
+    choose a per-replica microbatch per type."""
     lat = ProfiledLatency(profile["op_latency"])
-    plans = search(model, g, s, slo, lat, S_max=S_max, mus=mus, b_hats=b_hats)
+    plans = search(model, g, s, slo, lat, S_max=S_max, mus=mus, b_hats=b_hats, per_type_batch=per_type_batch)
     rows = []
     if plans:
         p = plans[0]
         rows.append(("search optimum", p))
+    tab = _Tables(model, g, s, lat, b_hats, 153e9)
     for label, r, q in named_plans(model):
+        S = len(q) - 1
+        combos = list(itertools.product(b_hats, repeat=S)) if per_type_batch and S > 1 else list(b_hats)
         best = None
         for mu in mus:
-            for b in b_hats:
-                p = _plan_from_tables(model, g, _Tables(model, g, s, lat, (b,), 153e9), q, mu, b, r)
+            for b in combos:
+                p = _plan_from_tables(model, g, tab, q, mu, b, r)
                 if p is not None and p.t_rtt <= slo and (best is None or p.cpt < best.cpt):
                     best = p
         if best is not None:
             rows.append((label, best))
     ops = [op.name for op in block_ops(model.block)]
-    out = [f"| plan | stages (operators, block rotated by r) | mu | b_hat | T_rtt ms | stage t_j us | "
+    out = [f"| plan | stages (operators, block rotated by r) | mu | b_hat per stage | T_rtt ms | stage t_j us | "
            f"GPU-seconds per 1k tokens |", "|---|---|---:|---:|---:|---|---:|"]
     for label, p in rows:
         N = len(ops)
         order = [ops[(p.rotation + i) % N] for i in range(N)]
         stages = " / ".join(f"{order[p.q[j]]}..{order[p.q[j + 1] - 1]}" for j in range(p.S))
-        out.append(f"| {label} | r={p.rotation}: {stages} | {p.mu} | {p.b_hat} | {p.t_rtt * 1e3:.2f} | "
-                   f"{', '.join(f'{t * 1e6:.0f}' for t in p.t)} | {p.cpt / g.c * 1e3:.3f} |")
+        out.append(f"| {label} | r={p.rotation}: {stages} | {p.mu} | {', '.join(str(b) for b in p.b_hats)} | "
+                   f"{p.t_rtt * 1e3:.2f} | {', '.join(f'{t * 1e6:.0f}' for t in p.t)} | {p.cpt / g.c * 1e3:.3f} |")
     return "\n".join(out)
 
 
@@ -479,13 +498,21 @@ if __name__ == "__main__":
     _sys.path.insert(0, _os.path.dirname(_os.path.dirname(_os.path.abspath(__file__))))
     import workloads as _W
 
-    ap = argparse.ArgumentParser(description="serving plans for the dense 8B-shaped model from a measured profile")
+    ap = argparse.ArgumentParser(description="serving plans for a model of repeated one-layer blocks from a "
+                                             "measured per-operator profile")
     ap.add_argument("--profile", required=True, help="JSON written by bench.py --latency-table")
+    ap.add_argument("--workload", default="dense8b_b64", help="one-layer workload whose layer the model repeats "
+                                                              "(the layer the profile was measured on)")
     ap.add_argument("--layers", type=int, default=32)
     ap.add_argument("--slo-ms", type=float, default=50.0)
+    ap.add_argument("--common-batch", action="store_true",
+                    help="one per-replica microbatch for every stage type (default: one per type for "
+                         "two-stage plans)")
     args = ap.parse_args()
     prof = json.load(open(args.profile))
-    model = Model(_W.BY_NAME["dense8b_b64"].layers, args.layers)
+    model = Model(_W.BY_NAME[args.workload].layers, args.layers)
+    b_hats = tuple(sorted({int(r["batch"]) for r in prof["op_latency"]}))
     for s in (1024, 4096, 16384):
         print(f"\n### context {s}, {args.layers} layers, TPOT SLO {args.slo_ms:g} ms, MI355X\n")
-        print(profile_report(prof, model, MI355X, s, args.slo_ms * 1e-3))
+        print(profile_report(prof, model, MI355X, s, args.slo_ms * 1e-3, b_hats=b_hats,
+                             per_type_batch=not args.common_batch))

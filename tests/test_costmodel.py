@@ -187,3 +187,76 @@ def test_profiled_latency_interpolates_between_measured_points():
     assert lat(op, 5, 1024) == pytest.approx(14e-6)
     assert lat(op, 5, 2560) == pytest.approx(21e-6)  # 14 us at 1024, 28 us at 4096
     assert lat(op, 100, 99999) == pytest.approx(36e-6)
+
+
+# ---------------------------------------------------------------- per-type microbatches (Appendix B replicas)
+
+MOE32 = CM.Model(W.BY_NAME["moe64x8_b512"].layers, 32)
+
+
+def test_equal_per_type_microbatches_give_the_common_plan():
+    g = CM.MI355X
+    for model, N in ((DENSE32, 10), (MOE32, 14)):
+        for s, q, mu, b, r in ((4096, (0, 6, N), 2, 64, 0), (16384, (0, N - 2, N), 4, 32, 5),
+                               (1024, (0, 3, 9, N), 1, 128, 2)):
+            one = CM.evaluate(model, g, q, mu, b, s, rotation=r)
+            tab = CM._Tables(model, g, s, CM.roofline_latency(g), (b,), 153e9)
+            per = CM._plan_from_tables(model, g, tab, q, mu, (b,) * (len(q) - 1), r)
+            assert (one is None) == (per is None)
+            if one is not None:
+                assert (per.t, per.u, per.t_rtt, per.cpt) == (one.t, one.u, one.t_rtt, one.cpt)
+                assert per.b_hats == (b,) * (len(q) - 1)
+
+
+def test_per_type_cost_counts_the_replicas():
+    """A global microbatch of B_hat requests takes B_hat / b_hat_m replicas of
+    type m; every replica is paid for T_rtt per round trip, which completes
+    mu * B_hat tokens (Appendix B, cost-per-token derivation)."""
+    g, s = CM.MI355X, 1024
+    tab = CM._Tables(MOE32, g, s, CM.roofline_latency(g), (64, 128, 1024), 153e9)
+    for bs, mu in (((128, 1024), 2), ((1024, 64), 1), ((64, 128), 4)):
+        p = CM._plan_from_tables(MOE32, g, tab, (0, 6, 14), mu, bs, 0)
+        assert p is not None and p.b_hats == bs and p.b_hat == max(bs)
+        B_hat = math.lcm(*bs)
+        replicas = [B_hat // b for b in bs]
+        gpu_seconds = p.t_rtt * g.c * sum(replicas)
+        assert p.cpt == pytest.approx(gpu_seconds / (mu * B_hat), rel=1e-12)
+
+
+def test_each_type_holds_the_kv_of_its_own_microbatches():
+    g, s = CM.MI355X, 16384  # 1 GB of KV per request over 32 layers
+    tab = CM._Tables(MOE32, g, s, CM.roofline_latency(g), (128, 512, 1024), 153e9)
+    # attention side at 512 requests needs 512 GB of KV: no plan, whatever the FFN side gathers
+    assert CM._plan_from_tables(MOE32, g, tab, (0, 6, 14), 1, (512, 128), 0) is None
+    p = CM._plan_from_tables(MOE32, g, tab, (0, 6, 14), 1, (128, 1024), 0)
+    assert p is not None and p.memory[0] <= g.memory and p.memory[1] <= g.memory
+    assert p.memory[1] == pytest.approx(MOE32.n_blocks * sum(
+        CM.op_bytes_flops(op.cfg, op.name, 1, s)[2] for op in CM.block_ops(MOE32.block)[6:]))
+
+
+def test_per_type_search_contains_the_common_one():
+    g, s = CM.MI355X, 4096
+    kw = dict(S_max=2, mus=(1, 2), b_hats=(32, 128, 512))
+    common = CM.search(DENSE32, g, s, slo=0.05, **kw)
+    per = CM.search(DENSE32, g, s, slo=0.05, per_type_batch=True, **kw)
+    assert per and per[0].cpt <= common[0].cpt
+    assert len(per) > len(common)
+
+
+def test_gathering_pays_only_where_the_colocated_batch_is_memory_bound():
+    """Theorem 1's regimes on the roofline latencies: while the colocated batch
+    can reach b* (short contexts) no disaggregated plan is cheaper; once memory
+    caps it below b*, a type that gathers several replicas' microbatches for
+    the expert GEMMs is."""
+    g = CM.MI355X
+    bs = (64, 128, 512, 1024, 2048, 4096)
+    assert CM.b_bar(g, MOE32, 256) > 2 * CM.b_star(g, MOE32) and CM.b_bar(g, MOE32, 16384) < CM.b_star(g, MOE32)
+    gains = {}
+    for s in (256, 16384):
+        col = CM.search(MOE32, g, s, slo=10.0, S_max=1, mus=(1,), b_hats=bs)[0]
+        best = CM.search(MOE32, g, s, slo=10.0, S_max=2, mus=(1, 2, 4), b_hats=bs, per_type_batch=True)[0]
+        gains[s] = col.cpt / best.cpt
+        if s == 16384:
+            assert best.S == 2 and len(set(best.b_hats)) == 2
+    assert gains[256] == pytest.approx(1.0)
+    assert gains[16384] > 1.2
