@@ -343,12 +343,14 @@ def ffn_sweep(args):
 def latency_table(args):
     """Profiled stage latencies t_j = f_lat(op range, batch, context), the
     per-stage inputs of the paper's communication-aware latency model (Section
-    4), for the layer of a one-layer workload (--workload: the dense 8B-shaped
-    layer by default, or the MoE layer): every single operator and every stage
+    4), for every distinct layer shape of a workload (--workload: the dense
+    8B-shaped layer by default, the MoE layer, or the hybrid block's
+    sliding-window and full layers): every single operator and every stage
     template at every (batch, context) point, the templates timed as a replay
     of their captured HIP graph and as an eager ods_run_partition call (median
     of --steps each). One weight/KV copy: small KV footprints partly stay in
-    the 256 MB last-level cache."""
+    the 256 MB last-level cache. Rows carry the layer's window (0: full
+    attention)."""
     import torch
     import workloads as W
     from workloads import gen
@@ -356,21 +358,9 @@ def latency_table(args):
     from paper_2609_14237_amd import runtime as R
 
     base = W.BY_NAME[args.workload]
-    if len(base.layers) != 1:
-        sys.exit("--latency-table profiles one layer shape: choose a one-layer workload")
-    cfg = base.layers[0]
-    n_ops = cfg.n_ops
+    shapes = list(dict.fromkeys(base.layers))  # distinct layer shapes, in block order
     dev = "cuda"
     torch.cuda.set_device(0)
-    templates = [("attention stage", 0, 6), ("FFN stage", 6, n_ops), ("core attention", 3, 5),
-                 ("colocated layer", 0, n_ops)]
-    # the MoE layer's expert GEMMs stay bound by their weight stream far past
-    # 256 rows (its b* is about 2000), so its table goes further
-    batches = (1, 8, 32, 64, 128, 256) + ((512, 1024) if cfg.n_experts else ())
-    weights = [gen.layer_weights(cfg, base.seed, 0, dev, base.router_std)]
-    tiled = args.weights == "tiled"
-    if tiled:
-        weights = [R.tile_weights(cfg, weights[0])]
     stream = torch.cuda.current_stream().cuda_stream
 
     def median_us(fn):
@@ -387,38 +377,51 @@ def latency_table(args):
         return float(np.median([a.elapsed_time(b) for a, b in evs])) * 1e3
 
     rows, op_rows = [], []
-    for ctx_len in (1024, 4096, 16384):
-        for M in batches:
-            ctx = np.full(M, ctx_len, dtype=np.int32)
-            P = gen.pool_pages_for(ctx)
-            max_pages = -(-ctx_len // 16)
-            table = np.zeros((M, max_pages), dtype=np.int32)
-            assert B.ods_kv_alloc(P, ctx, M, base.seed, max_pages, table) == 0, B.ods_last_error()
-            batch = R.DeviceBatch(torch.from_numpy(ctx).to(dev), torch.from_numpy(table).to(dev))
-            pools = [gen.kv_pool(cfg, P, base.seed, 0, dev)]
-            blk = R.DeviceBlock([cfg], weights, pools, P, pretiled=tiled)
-            st = R.DeviceState(blk, batch, dev)
-            x = gen.activations(M, cfg.hidden, base.seed, dev)
-            for i in range(n_ops):  # single operators, eager, for per-operator latency models
-                st.view("resid", M, cfg.hidden).copy_(x)
-                if i > 0:
-                    R.run_partition(blk, 0, i, batch, st, stream)
-                t_op = median_us(lambda: R.run_partition(blk, i, i + 1, batch, st, stream))
-                op_rows.append({"local": i, "name": blk.op_name(i), "batch": M, "ctx": ctx_len, "us": t_op})
-            for name, a, b in templates:
-                st.view("resid", M, cfg.hidden).copy_(x)
-                if a > 0:  # inputs of a later stage: run the layer up to it once
-                    R.run_partition(blk, 0, a, batch, st, stream)
-                t_eager = median_us(lambda: R.run_partition(blk, a, b, batch, st, stream))
-                g = R.PartitionGraph(blk, a, b, batch, st)
-                t_graph = median_us(lambda: g.launch(stream))
-                g.close()
-                rows.append({"stage": name, "op_range": [a, b], "batch": M, "ctx": ctx_len,
-                             "us_graph": t_graph, "us_eager": t_eager})
-                print(f"[latency] ctx {ctx_len} batch {M} {name} [{a},{b}): graph {t_graph:.1f} us, "
-                      f"eager {t_eager:.1f} us", file=sys.stderr, flush=True)
-            del blk, st, pools, batch
-            torch.cuda.empty_cache()
+    for cfg in shapes:
+        n_ops = cfg.n_ops
+        templates = [("attention stage", 0, 6), ("FFN stage", 6, n_ops), ("core attention", 3, 5),
+                     ("colocated layer", 0, n_ops)]
+        # the MoE layer's expert GEMMs stay bound by their weight stream far past
+        # 256 rows (its b* is about 2000), so its table goes further
+        batches = (1, 8, 32, 64, 128, 256) + ((512, 1024) if cfg.n_experts else ())
+        weights = [gen.layer_weights(cfg, base.seed, 0, dev, base.router_std)]
+        tiled = args.weights == "tiled"
+        if tiled:
+            weights = [R.tile_weights(cfg, weights[0])]
+        for ctx_len in (1024, 4096, 16384):
+            for M in batches:
+                ctx = np.full(M, ctx_len, dtype=np.int32)
+                P = gen.pool_pages_for(ctx)
+                max_pages = -(-ctx_len // 16)
+                table = np.zeros((M, max_pages), dtype=np.int32)
+                assert B.ods_kv_alloc(P, ctx, M, base.seed, max_pages, table) == 0, B.ods_last_error()
+                batch = R.DeviceBatch(torch.from_numpy(ctx).to(dev), torch.from_numpy(table).to(dev))
+                pools = [gen.kv_pool(cfg, P, base.seed, 0, dev)]
+                blk = R.DeviceBlock([cfg], weights, pools, P, pretiled=tiled)
+                st = R.DeviceState(blk, batch, dev)
+                x = gen.activations(M, cfg.hidden, base.seed, dev)
+                for i in range(n_ops):  # single operators, eager, for per-operator latency models
+                    st.view("resid", M, cfg.hidden).copy_(x)
+                    if i > 0:
+                        R.run_partition(blk, 0, i, batch, st, stream)
+                    t_op = median_us(lambda: R.run_partition(blk, i, i + 1, batch, st, stream))
+                    op_rows.append({"local": i, "name": blk.op_name(i), "window": cfg.window, "batch": M,
+                                    "ctx": ctx_len, "us": t_op})
+                for name, a, b in templates:
+                    st.view("resid", M, cfg.hidden).copy_(x)
+                    if a > 0:  # inputs of a later stage: run the layer up to it once
+                        R.run_partition(blk, 0, a, batch, st, stream)
+                    t_eager = median_us(lambda: R.run_partition(blk, a, b, batch, st, stream))
+                    g = R.PartitionGraph(blk, a, b, batch, st)
+                    t_graph = median_us(lambda: g.launch(stream))
+                    g.close()
+                    rows.append({"stage": name, "op_range": [a, b], "window": cfg.window, "batch": M,
+                                 "ctx": ctx_len, "us_graph": t_graph, "us_eager": t_eager})
+                    print(f"[latency] window {cfg.window} ctx {ctx_len} batch {M} {name} [{a},{b}): graph "
+                          f"{t_graph:.1f} us, eager {t_eager:.1f} us", file=sys.stderr, flush=True)
+                del blk, st, pools, batch
+                torch.cuda.empty_cache()
+        del weights
     print(json.dumps({"metric": "stage latency t_j = f_lat(op range, batch, context)", "workload": base.name,
                       "layer": base.description, "unit": "us", "steps": args.steps, "warmup": args.warmup, "dtype": "bf16",
                       "data": "synthetic", "weight_layout": args.weights, "latency_table": rows,

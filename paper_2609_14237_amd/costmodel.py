@@ -18,8 +18,12 @@ x* = 2 P_act (gamma_1 - gamma_2) / (alpha_2 - alpha_1) of x = m_kv(s).
 
 Planner (Sections 4-5, Appendix B). A partition block of N ordered operators
 is cut by a contiguous template q = (0 = q_0 < ... < q_S = N); stage j runs on
-owner type sigma(j) = ((j - 1) mod K) + 1 (here K = S, one stage position per
-type). Each type m has its own per-replica microbatch b_hat_m, so a global
+owner type sigma(j) = ((j - 1) mod K) + 1: K = S (one stage position per type)
+for templates over the whole block, or, for a block of identical-structure
+layers, one per-layer template of K stages tiled over every layer (S = layers
+x K, each type owning one position per layer, as AFD and CAD do). Busy time,
+memory and link load add up over a type's positions. Each type m has its own
+per-replica microbatch b_hat_m, so a global
 microbatch of B_hat requests takes n_m = B_hat / b_hat_m replicas of type m:
 a type with a larger microbatch gathers the microbatches of several replicas
 of the types before it (Appendix B, replica counts). Stage latency t_j sums
@@ -290,14 +294,16 @@ def roofline_latency(g: Gpu) -> Callable:
 
 
 class ProfiledLatency:
-    """Measured single-operator latencies t(op, b, s) of one layer shape,
-    interpolated linearly in batch and sequence length (clamped at the ends).
-    rows: iterable of dicts with keys local (operator index), batch, ctx, us."""
+    """Measured single-operator latencies t(op, b, s) per layer shape (the
+    layer's attention window: 0 for full attention), interpolated linearly in
+    batch and sequence length (clamped at the ends). rows: iterable of dicts
+    with keys local (operator index), batch, ctx, us and optionally window."""
 
     def __init__(self, rows):
         table = {}
         for r in rows:
-            table.setdefault(int(r["local"]), {}).setdefault(float(r["ctx"]), []).append((float(r["batch"]), float(r["us"])))
+            key = (int(r.get("window", 0)), int(r["local"]))
+            table.setdefault(key, {}).setdefault(float(r["ctx"]), []).append((float(r["batch"]), float(r["us"])))
         self.table = {j: {c: sorted(v) for c, v in per.items()} for j, per in table.items()}
 
     @staticmethod
@@ -312,7 +318,7 @@ class ProfiledLatency:
         return y0 + (y1 - y0) * (x - x0) / (x1 - x0)
 
     def __call__(self, op: BlockOp, b: float, s: float) -> float:
-        per = self.table[op.local]
+        per = self.table[(int(getattr(op.cfg, "window", 0)), op.local)]
         ctxs = sorted(per)
         i = bisect.bisect_left(ctxs, s)
         if i == 0 or i == len(ctxs):
@@ -358,8 +364,14 @@ class Plan:
     u: list
     t_rtt: float
     cpt: float
-    memory: list = field(default_factory=list)
-    b_hats: tuple = ()    # per-replica microbatch of each stage's type
+    memory: list = field(default_factory=list)   # per type
+    b_hats: tuple = ()    # per-replica microbatch of each type
+    K: int = 0            # device-group types; stage j runs on type j mod K (0: one type per stage)
+    tiled: int = 0        # > 0: q tiles one per-layer template over this many layers
+
+    @property
+    def types(self) -> int:
+        return self.K or self.S
 
     @property
     def S(self) -> int:
@@ -383,28 +395,37 @@ class _Tables:
             self.by_b[b] = (pre(lat), pre(w), pre(kv), hand)
 
 
-def _plan_from_tables(model: Model, g: Gpu, tab: _Tables, q: tuple, mu: int, b_hat, rotation: int):
-    """b_hat: one per-replica microbatch for every type, or a tuple with one per stage."""
+def _plan_from_tables(model: Model, g: Gpu, tab: _Tables, q: tuple, mu: int, b_hat, rotation: int,
+                      K: int = 0, tiled: int = 0):
+    """Stage j of template q runs on device-group type j mod K (K = 0: one
+    type per stage, K = S). b_hat: one per-replica microbatch for every type,
+    or a tuple with one per type."""
     S = len(q) - 1
-    bs = tuple(b_hat) if isinstance(b_hat, tuple) else (b_hat,) * S
-    t, u, mem = [], [], []
+    T = K or S
+    if S % T:
+        raise ValueError("the stages must fill every type the same number of times")
+    bs = tuple(b_hat) if isinstance(b_hat, tuple) else (b_hat,) * T
+    t, u = [], []
+    mem = [0.0] * T
     for j in range(S):
-        plat, pw, pkv, _ = tab.by_b[bs[j]]
+        m, m_next = j % T, (j + 1) % S % T
+        plat, pw, pkv, _ = tab.by_b[bs[m]]
         lo, hi = rotation + q[j], rotation + q[j + 1]
         t.append(plat[hi] - plat[lo])
-        u.append(tab.by_b[max(bs[j], bs[(j + 1) % S])][3][hi - 1] if S > 1 else 0.0)
-        need = (pw[hi] - pw[lo]) * model.n_blocks + mu * bs[j] * (pkv[hi] - pkv[lo]) * model.n_blocks
-        if need > g.memory:
-            return None
-        mem.append(need)
+        # the live set crosses to the next stage's type (none when it stays on one replica)
+        u.append(tab.by_b[max(bs[m], bs[m_next])][3][hi - 1] if m != m_next else 0.0)
+        mem[m] += (pw[hi] - pw[lo]) * model.n_blocks + mu * bs[m] * (pkv[hi] - pkv[lo]) * model.n_blocks
+    if any(x > g.memory for x in mem):
+        return None
     Bt = model.n_blocks
-    chain = Bt * sum(t) + Bt * sum(u) - (u[-1] if S > 1 else 0.0)
-    loads = [mu * Bt * tj for tj in t] + [mu * Bt * uj for uj in u[:-1]]
-    if S > 1:
-        loads.append(mu * (Bt - 1) * u[-1])
+    chain = Bt * sum(t) + Bt * sum(u) - u[-1]
+    busy = [sum(t[j] for j in range(m, S, T)) for m in range(T)]
+    link = [sum(u[j] for j in range(m, S, T)) for m in range(T)]
+    loads = [mu * Bt * x for x in busy] + [mu * Bt * x - (mu * u[-1] if m == (S - 1) % T else 0.0)
+                                           for m, x in enumerate(link)]
     t_rtt = max([chain] + loads)
     cpt = t_rtt * sum(g.c / (mu * b) for b in bs)
-    return Plan(rotation, q, mu, max(bs), t, u, t_rtt, cpt, mem, bs)
+    return Plan(rotation, q, mu, max(bs), t, u, t_rtt, cpt, mem, bs, K, tiled)
 
 
 def evaluate(model: Model, g: Gpu, q: tuple, mu: int, b_hat: int, s: float, latency: Callable | None = None,
@@ -416,28 +437,47 @@ def evaluate(model: Model, g: Gpu, q: tuple, mu: int, b_hat: int, s: float, late
     return _plan_from_tables(model, g, tab, q, mu, b_hat, rotation)
 
 
+def layer_ops_count(model: Model) -> int:
+    """Operators per layer when every layer of the block has the same count, else 0."""
+    counts = {len(layer_op_names(c)) for c in model.block}
+    return counts.pop() if len(counts) == 1 else 0
+
+
 def search(model: Model, g: Gpu, s: float, slo: float, latency: Callable | None = None, S_max: int = 3,
            mus=(1, 2, 4, 8), b_hats=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), link_bw: float = 153e9,
-           rotations: bool = True, per_type_batch: bool = False, per_type_S_max: int = 2):
+           rotations: bool = True, per_type_batch: bool = False, per_type_S_max: int = 2, tiled_K=(2, 3)):
     """Every plan over the grid that meets the SLO and fits memory, cheapest
-    first. With per_type_batch, plans of 2 to per_type_S_max stages also try
-    every combination of per-replica microbatches over their types."""
+    first: contiguous templates of 1 to S_max stages over the block, one type
+    per stage, and, for a block of several layers with the same operator
+    sequence, one per-layer template of K stages tiled over every layer, its
+    stages placed round-robin on K types (S = layers x K). With
+    per_type_batch, plans of up to per_type_S_max types also try every
+    combination of per-replica microbatches over their types."""
     tab = _Tables(model, g, s, latency or roofline_latency(g), b_hats, link_bw)
     N = tab.N
+
+    def combos(T):
+        return list(itertools.product(b_hats, repeat=T)) if per_type_batch and 1 < T <= per_type_S_max else list(b_hats)
+
     out = []
+
+    def consider(q, r, K, tiled):
+        for mu in mus:
+            for b in combos(K or len(q) - 1):
+                p = _plan_from_tables(model, g, tab, q, mu, b, r, K, tiled)
+                if p is not None and p.t_rtt <= slo:
+                    out.append(p)
+
     for S in range(1, S_max + 1):
-        rots = range(N) if (rotations and S > 1) else (0,)
-        if per_type_batch and 1 < S <= per_type_S_max:
-            combos = list(itertools.product(b_hats, repeat=S))
-        else:
-            combos = list(b_hats)
-        for r in rots:
+        for r in (range(N) if (rotations and S > 1) else (0,)):
             for q in templates(N, S):
-                for mu in mus:
-                    for b in combos:
-                        p = _plan_from_tables(model, g, tab, q, mu, b, r)
-                        if p is not None and p.t_rtt <= slo:
-                            out.append(p)
+                consider(q, r, 0, 0)
+    L, n = layer_ops_count(model), len(model.block)
+    if L and n > 1:
+        for K in tiled_K:
+            for r in (range(L) if rotations else (0,)):
+                for q in subblock_templates(N, n, K):
+                    consider(q, r, K, n)
     out.sort(key=lambda p: p.cpt)
     return out
 
@@ -445,12 +485,18 @@ def search(model: Model, g: Gpu, s: float, slo: float, latency: Callable | None 
 # ---------------------------------------------------------------- plans from a measured profile
 
 def named_plans(model: Model):
-    """(label, rotation, q) of the two-way templates the paper names, for a
-    one-layer dense or MoE block: AFD cuts after the output projection; CAD
-    isolates core attention (kv_append, attn_core) and lets the rest-of-model
-    stage wrap the block boundary; colocated is one stage."""
+    """(label, rotation, q, K, tiled) of the templates the paper names: AFD
+    cuts every layer after its output projection, CAD isolates every layer's
+    core attention (kv_append, attn_core) and lets the rest-of-model stage wrap
+    the layer boundary (a rotation by five operators); both alternate two
+    device-group types over the block's layers. Colocated is one stage."""
     N = len(block_ops(model.block))
-    return [("colocated", 0, (0, N)), ("AFD", 0, (0, 6, N)), ("CAD", 5, (0, N - 2, N))]
+    n = len(model.block)
+    if n == 1 or not layer_ops_count(model):
+        return [("colocated", 0, (0, N), 0, 0), ("AFD", 0, (0, 6, N), 0, 0), ("CAD", 5, (0, N - 2, N), 0, 0)]
+    L = layer_ops_count(model)
+    tile = lambda sub: tuple([0] + [r * L + x for r in range(n) for x in sub[1:]])
+    return [("colocated", 0, (0, N), 0, 0), ("AFD", 0, tile((0, 6, L)), 2, n), ("CAD", 5, tile((0, L - 2, L)), 2, n)]
 
 
 def profile_report(profile: dict, model: Model, g: Gpu, s: float, slo: float, S_max: int = 3,
@@ -466,26 +512,37 @@ def profile_report(profile: dict, model: Model, g: Gpu, s: float, slo: float, S_
         p = plans[0]
         rows.append(("search optimum", p))
     tab = _Tables(model, g, s, lat, b_hats, 153e9)
-    for label, r, q in named_plans(model):
-        S = len(q) - 1
-        combos = list(itertools.product(b_hats, repeat=S)) if per_type_batch and S > 1 else list(b_hats)
+    for label, r, q, K, tiled in named_plans(model):
+        T = K or len(q) - 1
+        combos = list(itertools.product(b_hats, repeat=T)) if per_type_batch and T > 1 else list(b_hats)
         best = None
         for mu in mus:
             for b in combos:
-                p = _plan_from_tables(model, g, tab, q, mu, b, r)
+                p = _plan_from_tables(model, g, tab, q, mu, b, r, K, tiled)
                 if p is not None and p.t_rtt <= slo and (best is None or p.cpt < best.cpt):
                     best = p
         if best is not None:
             rows.append((label, best))
-    ops = [op.name for op in block_ops(model.block)]
-    out = [f"| plan | stages (operators, block rotated by r) | mu | b_hat per stage | T_rtt ms | stage t_j us | "
+    return _plan_table(model, g, rows)
+
+
+def _plan_table(model: Model, g: Gpu, rows) -> str:
+    bops = block_ops(model.block)
+    N = len(bops)
+    name = lambda i: (f"L{bops[i % N].layer}." if len(model.block) > 1 else "") + bops[i % N].name
+    out = [f"| plan | stages (operators, block rotated by r) | mu | b_hat per type | T_rtt ms | busy per type us | "
            f"GPU-seconds per 1k tokens |", "|---|---|---:|---:|---:|---|---:|"]
     for label, p in rows:
-        N = len(ops)
-        order = [ops[(p.rotation + i) % N] for i in range(N)]
-        stages = " / ".join(f"{order[p.q[j]]}..{order[p.q[j + 1] - 1]}" for j in range(p.S))
+        if p.tiled:
+            per = p.S // p.tiled
+            stages = (" / ".join(f"{name(p.rotation + p.q[j])}..{name(p.rotation + p.q[j + 1] - 1)}"
+                                 for j in range(per)) + f" (every layer, {p.types} types)")
+        else:
+            stages = " / ".join(f"{name(p.rotation + p.q[j])}..{name(p.rotation + p.q[j + 1] - 1)}"
+                                for j in range(p.S))
+        busy = [sum(p.t[j] for j in range(m, p.S, p.types)) for m in range(p.types)]
         out.append(f"| {label} | r={p.rotation}: {stages} | {p.mu} | {', '.join(str(b) for b in p.b_hats)} | "
-                   f"{p.t_rtt * 1e3:.2f} | {', '.join(f'{t * 1e6:.0f}' for t in p.t)} | {p.cpt / g.c * 1e3:.3f} |")
+                   f"{p.t_rtt * 1e3:.2f} | {', '.join(f'{t * 1e6:.0f}' for t in busy)} | {p.cpt / g.c * 1e3:.3f} |")
     return "\n".join(out)
 
 
@@ -510,7 +567,10 @@ if __name__ == "__main__":
                          "two-stage plans)")
     args = ap.parse_args()
     prof = json.load(open(args.profile))
-    model = Model(_W.BY_NAME[args.workload].layers, args.layers)
+    block = _W.BY_NAME[args.workload].layers
+    if args.layers % len(block):
+        _sys.exit(f"--layers must be a multiple of the block's {len(block)} layers")
+    model = Model(block, args.layers // len(block))
     b_hats = tuple(sorted({int(r["batch"]) for r in prof["op_latency"]}))
     for s in (1024, 4096, 16384):
         print(f"\n### context {s}, {args.layers} layers, TPOT SLO {args.slo_ms:g} ms, MI355X\n")

@@ -260,3 +260,55 @@ def test_gathering_pays_only_where_the_colocated_batch_is_memory_bound():
             assert best.S == 2 and len(set(best.b_hats)) == 2
     assert gains[256] == pytest.approx(1.0)
     assert gains[16384] > 1.2
+
+
+# ---------------------------------------------------------------- per-layer templates over several device-group types
+
+def test_tiled_plan_is_the_same_deployment_as_the_one_layer_block():
+    """Four identical layers per block, AFD cut in every layer, stages
+    alternating over two types, eight blocks: the same deployment as a
+    one-layer block cut once over 32 blocks, so the same round trip, memory
+    and cost."""
+    g, s = CM.MI355X, 4096
+    layer = W.BY_NAME["dense8b_b64"].layers[0]
+    four = CM.Model((layer,) * 4, 8)
+    label, r, q, K, tiled = [p for p in CM.named_plans(four) if p[0] == "AFD"][0]
+    assert (r, q, K, tiled) == (0, (0, 6, 10, 16, 20, 26, 30, 36, 40), 2, 4)
+    for mu, bs in ((1, (64, 64)), (2, (32, 128)), (4, (128, 8))):
+        t4 = CM._Tables(four, g, s, CM.roofline_latency(g), set(bs), 153e9)
+        t1 = CM._Tables(DENSE32, g, s, CM.roofline_latency(g), set(bs), 153e9)
+        a = CM._plan_from_tables(four, g, t4, q, mu, bs, r, K, tiled)
+        b = CM._plan_from_tables(DENSE32, g, t1, (0, 6, 10), mu, bs, 0)
+        assert a is not None and b is not None and a.types == b.types == 2
+        assert a.t_rtt == pytest.approx(b.t_rtt, rel=1e-12)
+        assert a.cpt == pytest.approx(b.cpt, rel=1e-12)
+        assert a.memory == pytest.approx(b.memory, rel=1e-12)
+
+
+def test_tiled_plan_sums_each_type_over_the_layers():
+    g, s = CM.MI355X, 16384
+    m = CM.Model(W.BY_NAME["hybrid4_b128"].layers, 8)
+    lat = CM.roofline_latency(g)
+    ops = CM.block_ops(m.block)
+    label, r, q, K, tiled = [p for p in CM.named_plans(m) if p[0] == "CAD"][0]
+    assert (r, K, tiled) == (5, 2, 4) and len(q) == 9
+    tab = CM._Tables(m, g, s, lat, (16, 64), 153e9)
+    p = CM._plan_from_tables(m, g, tab, q, 2, (64, 16), r, K, tiled)
+    core = [i for i, op in enumerate(ops) if op.name in ("kv_append", "attn_core")]
+    rest = [i for i in range(len(ops)) if i not in core]
+    busy = [sum(p.t[j] for j in range(mm, p.S, 2)) for mm in range(2)]
+    assert busy[0] == pytest.approx(sum(lat(ops[i], 64, s) for i in rest), rel=1e-12)
+    assert busy[1] == pytest.approx(sum(lat(ops[i], 16, s) for i in core), rel=1e-12)
+    kv = sum(CM.op_bytes_flops(ops[i].cfg, ops[i].name, 1, s)[3] for i in core)
+    assert p.memory[1] == pytest.approx(2 * 16 * kv * m.n_blocks, rel=1e-12)  # core attention holds all the KV
+    assert p.cpt == pytest.approx(p.t_rtt * g.c * (1 / (2 * 64) + 1 / (2 * 16)), rel=1e-12)
+
+
+def test_profiled_latency_keeps_window_and_full_layers_apart():
+    rows = [{"local": 4, "window": 0, "batch": 8, "ctx": 16384, "us": 100.0},
+            {"local": 4, "window": 1024, "batch": 8, "ctx": 16384, "us": 10.0}]
+    lat = CM.ProfiledLatency(rows)
+    ops = CM.block_ops(W.BY_NAME["hybrid4_b128"].layers)
+    swa, full = ops[4], ops[34]
+    assert (swa.name, full.name, swa.cfg.window, full.cfg.window) == ("attn_core", "attn_core", 1024, 0)
+    assert lat(swa, 8, 16384) == pytest.approx(10e-6) and lat(full, 8, 16384) == pytest.approx(100e-6)
