@@ -41,7 +41,9 @@ b_m = mu * b_hat_m, subject to T_rtt <= SLO and, per type, weights of its
 stages plus the KV of mu resident microbatches within M. The search is
 exhaustive over S, templates (and the block's rotation, so a stage may wrap
 the block boundary as CAD's rest-of-model stage does), mu and the
-microbatches: one shared by every type, or (per_type_batch) one per type.
+microbatches: one shared by every type, or (per_type_batch) one per type;
+given several GPU kinds, every type also takes any kind, each with its own
+price, memory and latencies (heterogeneous plans).
 """
 from __future__ import annotations
 
@@ -368,6 +370,7 @@ class Plan:
     b_hats: tuple = ()    # per-replica microbatch of each type
     K: int = 0            # device-group types; stage j runs on type j mod K (0: one type per stage)
     tiled: int = 0        # > 0: q tiles one per-layer template over this many layers
+    kinds: tuple = ()     # GPU kind of each type
 
     @property
     def types(self) -> int:
@@ -395,27 +398,30 @@ class _Tables:
             self.by_b[b] = (pre(lat), pre(w), pre(kv), hand)
 
 
-def _plan_from_tables(model: Model, g: Gpu, tab: _Tables, q: tuple, mu: int, b_hat, rotation: int,
+def _plan_from_tables(model: Model, g, tab, q: tuple, mu: int, b_hat, rotation: int,
                       K: int = 0, tiled: int = 0):
     """Stage j of template q runs on device-group type j mod K (K = 0: one
     type per stage, K = S). b_hat: one per-replica microbatch for every type,
-    or a tuple with one per type."""
+    or a tuple with one per type. g, tab: one GPU kind (and its tables) for
+    every type, or tuples with one per type (heterogeneous plans)."""
     S = len(q) - 1
     T = K or S
     if S % T:
         raise ValueError("the stages must fill every type the same number of times")
     bs = tuple(b_hat) if isinstance(b_hat, tuple) else (b_hat,) * T
+    gs = tuple(g) if isinstance(g, (tuple, list)) else (g,) * T
+    tabs = tuple(tab) if isinstance(tab, (tuple, list)) else (tab,) * T
     t, u = [], []
     mem = [0.0] * T
     for j in range(S):
         m, m_next = j % T, (j + 1) % S % T
-        plat, pw, pkv, _ = tab.by_b[bs[m]]
+        plat, pw, pkv, _ = tabs[m].by_b[bs[m]]
         lo, hi = rotation + q[j], rotation + q[j + 1]
         t.append(plat[hi] - plat[lo])
         # the live set crosses to the next stage's type (none when it stays on one replica)
-        u.append(tab.by_b[max(bs[m], bs[m_next])][3][hi - 1] if m != m_next else 0.0)
+        u.append(tabs[m].by_b[max(bs[m], bs[m_next])][3][hi - 1] if m != m_next else 0.0)
         mem[m] += (pw[hi] - pw[lo]) * model.n_blocks + mu * bs[m] * (pkv[hi] - pkv[lo]) * model.n_blocks
-    if any(x > g.memory for x in mem):
+    if any(x > gm.memory for x, gm in zip(mem, gs)):
         return None
     Bt = model.n_blocks
     chain = Bt * sum(t) + Bt * sum(u) - u[-1]
@@ -424,8 +430,8 @@ def _plan_from_tables(model: Model, g: Gpu, tab: _Tables, q: tuple, mu: int, b_h
     loads = [mu * Bt * x for x in busy] + [mu * Bt * x - (mu * u[-1] if m == (S - 1) % T else 0.0)
                                            for m, x in enumerate(link)]
     t_rtt = max([chain] + loads)
-    cpt = t_rtt * sum(g.c / (mu * b) for b in bs)
-    return Plan(rotation, q, mu, max(bs), t, u, t_rtt, cpt, mem, bs, K, tiled)
+    cpt = t_rtt * sum(gm.c / (mu * b) for gm, b in zip(gs, bs))
+    return Plan(rotation, q, mu, max(bs), t, u, t_rtt, cpt, mem, bs, K, tiled, tuple(gm.name for gm in gs))
 
 
 def evaluate(model: Model, g: Gpu, q: tuple, mu: int, b_hat: int, s: float, latency: Callable | None = None,
@@ -443,7 +449,7 @@ def layer_ops_count(model: Model) -> int:
     return counts.pop() if len(counts) == 1 else 0
 
 
-def search(model: Model, g: Gpu, s: float, slo: float, latency: Callable | None = None, S_max: int = 3,
+def search(model: Model, g, s: float, slo: float, latency=None, S_max: int = 3,
            mus=(1, 2, 4, 8), b_hats=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), link_bw: float = 153e9,
            rotations: bool = True, per_type_batch: bool = False, per_type_S_max: int = 2, tiled_K=(2, 3)):
     """Every plan over the grid that meets the SLO and fits memory, cheapest
@@ -452,9 +458,20 @@ def search(model: Model, g: Gpu, s: float, slo: float, latency: Callable | None 
     sequence, one per-layer template of K stages tiled over every layer, its
     stages placed round-robin on K types (S = layers x K). With
     per_type_batch, plans of up to per_type_S_max types also try every
-    combination of per-replica microbatches over their types."""
-    tab = _Tables(model, g, s, latency or roofline_latency(g), b_hats, link_bw)
-    N = tab.N
+    combination of per-replica microbatches over their types. g is one GPU
+    kind or a sequence of kinds, in which case every type takes any of them
+    (the heterogeneous plans of Section 3.3); latency is one callable for
+    every kind or a dict from kind name to callable (default: each kind's
+    roofline)."""
+    kinds = tuple(g) if isinstance(g, (tuple, list)) else (g,)
+
+    def lat_of(k):
+        if isinstance(latency, dict):
+            return latency[k.name]
+        return latency or roofline_latency(k)
+
+    tabs = {k.name: _Tables(model, k, s, lat_of(k), b_hats, link_bw) for k in kinds}
+    N = next(iter(tabs.values())).N
 
     def combos(T):
         return list(itertools.product(b_hats, repeat=T)) if per_type_batch and 1 < T <= per_type_S_max else list(b_hats)
@@ -462,11 +479,14 @@ def search(model: Model, g: Gpu, s: float, slo: float, latency: Callable | None 
     out = []
 
     def consider(q, r, K, tiled):
-        for mu in mus:
-            for b in combos(K or len(q) - 1):
-                p = _plan_from_tables(model, g, tab, q, mu, b, r, K, tiled)
-                if p is not None and p.t_rtt <= slo:
-                    out.append(p)
+        T = K or len(q) - 1
+        for ks in itertools.product(kinds, repeat=T):
+            tk = tuple(tabs[k.name] for k in ks)
+            for mu in mus:
+                for b in combos(T):
+                    p = _plan_from_tables(model, ks, tk, q, mu, b, r, K, tiled)
+                    if p is not None and p.t_rtt <= slo:
+                        out.append(p)
 
     for S in range(1, S_max + 1):
         for r in (range(N) if (rotations and S > 1) else (0,)):

@@ -312,3 +312,53 @@ def test_profiled_latency_keeps_window_and_full_layers_apart():
     swa, full = ops[4], ops[34]
     assert (swa.name, full.name, swa.cfg.window, full.cfg.window) == ("attn_core", "attn_core", 1024, 0)
     assert lat(swa, 8, 16384) == pytest.approx(10e-6) and lat(full, 8, 16384) == pytest.approx(100e-6)
+
+
+# ---------------------------------------------------------------- heterogeneous plans (a GPU kind per type)
+
+def test_one_kind_is_the_homogeneous_search():
+    g, s = CM.MI355X, 4096
+    kw = dict(S_max=2, mus=(1, 2), b_hats=(32, 128, 256), per_type_batch=True)
+    a = CM.search(DENSE32, g, s, 0.05, **kw)
+    b = CM.search(DENSE32, (g,), s, 0.05, **kw)
+    assert [p.cpt for p in a] == [p.cpt for p in b] and set(b[0].kinds) == {"MI355X"}
+
+
+def test_a_dominated_kind_is_never_chosen():
+    """Theorem 2's dominance case: a kind costlier per byte and per flop (with
+    the same memory) never lowers a plan's cost, so the cheapest plan uses
+    only the dominant kind."""
+    gpus, _ = paper_gpus()
+    a = gpus["H100"]
+    b = CM.Gpu("H100x", a.price_per_hour * 1.3, a.bandwidth * 0.9, a.memory, a.flops * 0.95)
+    assert b.alpha > a.alpha and b.gamma > a.gamma
+    for s in (1024, 16384):
+        kw = dict(S_max=2, mus=(1, 2, 4), b_hats=(8, 64, 256), per_type_batch=True)
+        hom = CM.search(DENSE32, a, s, 0.2, **kw)[0]
+        het = CM.search(DENSE32, (a, b), s, 0.2, **kw)[0]
+        assert set(het.kinds) == {"H100"} and het.cpt == pytest.approx(hom.cpt, rel=1e-12)
+
+
+def test_complementary_kinds_split_attention_from_the_gemms():
+    """H100 with A100 (the paper's pair, eta = 1.93): A100 is cheaper per byte,
+    H100 per flop. The cheapest plan puts the KV-bound core attention on A100
+    and the GEMM operators on H100, beats either kind alone, and stays within
+    Theorem 2's (1 + sqrt(eta)) / 2."""
+    gpus, pairs = paper_gpus()
+    h, a = gpus["H100"], gpus["A100"]
+    assert a.alpha < h.alpha and h.gamma < a.gamma
+    bound = CM.g_het_bound(CM.eta(h, a))
+    ops = CM.block_ops(DENSE32.block)
+    for s in (1024, 4096):
+        kw = dict(S_max=2, mus=(1, 2, 4, 8), b_hats=(8, 32, 64, 128, 256, 512), per_type_batch=True)
+        best_hom = min(CM.search(DENSE32, k, s, 1.0, **kw)[0].cpt for k in (h, a))
+        het = CM.search(DENSE32, (h, a), s, 1.0, **kw)[0]
+        assert 1.05 < best_hom / het.cpt <= bound
+        assert set(het.kinds) == {"H100", "A100"}
+        for j in range(het.S):
+            names = {ops[(het.rotation + i) % len(ops)].name for i in range(het.q[j], het.q[j + 1])}
+            kind = het.kinds[j % het.types]
+            if "attn_core" in names:
+                assert kind == "A100"
+            if names & {"qkv_proj", "o_proj_residual", "gate_up", "down_residual"}:
+                assert kind == "H100"
