@@ -244,6 +244,58 @@ static void check_stream_tiles() {
   }
 }
 
+// Random layer shapes the library accepts (dense and MoE, full and sliding-
+// window attention, row-major and tiled weights, batches 1 to 700): every
+// operator range validates and plans as above, and the streaming GEMM's tile
+// and split choices stay inside what its launcher takes.
+static void check_random_shapes() {
+  std::mt19937_64 rng(11);
+  auto pick = [&](std::initializer_list<int> v) { return *(v.begin() + rng() % v.size()); };
+  for (int rep = 0; rep < 60; ++rep) {
+    const int D = pick({64, 128}), group = pick({1, 2, 4, 8, 16}), n_kv = pick({1, 2, 4, 8});
+    const bool moe = rng() % 3 == 0;
+    ods_layer L;
+    memset(&L, 0, sizeof(L));
+    ods_layer_cfg &c = L.cfg;
+    c.hidden = 64 * (2 + (int)(rng() % 40)) + (rng() % 4 == 0 ? 8 * (int)(1 + rng() % 7) : 0);
+    c.n_q = group * n_kv;
+    c.n_kv = n_kv;
+    c.head_dim = D;
+    c.window = rng() % 3 == 0 ? 16 * (int)(1 + rng() % 64) + (int)(rng() % 16) : 0;
+    if (moe) {
+      c.n_experts = pick({8, 16, 64, 128});
+      c.top_k = 1 + (int)(rng() % std::min(8, c.n_experts));
+      c.moe_ffn = 64 * (1 + (int)(rng() % 24)) + (rng() % 4 == 0 ? 8 : 0);
+    } else {
+      c.ffn = 64 * (1 + (int)(rng() % 200)) + (rng() % 4 == 0 ? 8 * (int)(1 + rng() % 7) : 0);
+    }
+    c.rope_theta = 10000.f;
+    c.rms_eps = 1e-6f;
+    L.g_attn = L.w_qkv = L.w_o = L.g_ffn = L.w_gate_up = L.w_down = L.w_router = kFake;
+    L.kv_pool = kFake;
+    L.pool_pages = 1000;
+    Work w{"random", 1 + (int)(rng() % 700), 1 + (int)(rng() % 300), {L}};
+    for (int tiled = 0; tiled < 2; ++tiled) {
+      w.layers[0].weight_layout = tiled ? ODS_WEIGHTS_TILED : ODS_WEIGHTS_ROWS;
+      const ods_block blk{1, w.layers.data()};
+      CHECK(check_block(&blk) == ODS_OK || (tiled && check_block(&blk) == ODS_EUNSUPPORTED));
+      if (check_block(&blk) != ODS_OK) continue;
+      check_block_ranges(w, 256);
+    }
+  }
+  for (int rep = 0; rep < 20000; ++rep) {
+    const int M = 1 + (int)(rng() % 4096), N = 8 * (1 + (int)(rng() % 4096)), K = 64 * (1 + (int)(rng() % 256));
+    const int epi = (int)(rng() % 4);
+    const int rows = gemm_stream_rows(M, N, K, epi), s = gemm_stream_splits(M, N, K, epi);
+    CHECK(rows == 64 || rows == 256);
+    CHECK(M > 64 || rows == 64);
+    CHECK(s == 1 || s == 2 || s == 4 || s == 8);
+    CHECK(s == 1 || K / 64 / s >= 8);  // every split keeps at least 8 K steps
+    const int tiles = (M + rows - 1) / rows * (epi == EPI_SILU ? (N + 63) / 64 : (N + 127) / 128);
+    CHECK(s == 1 || tiles * s <= 256);  // split-K never spills into a second wave
+  }
+}
+
 int main(int argc, char **argv) {
   if (argc < 2) {
     fprintf(stderr, "usage: host_check workloads.txt\n");
@@ -252,6 +304,7 @@ int main(int argc, char **argv) {
   check_allocator();
   check_bad_configs();
   check_stream_tiles();
+  check_random_shapes();
   for (Work &w : read_works(argv[1])) {
     for (int tiled = 0; tiled < 2; ++tiled) {
       for (ods_layer &L : w.layers) L.weight_layout = tiled ? ODS_WEIGHTS_TILED : ODS_WEIGHTS_ROWS;
